@@ -1,0 +1,166 @@
+"""fp64 CPU oracle for mini-batch SGD on the d-h-1 ReLU/MSE network.
+
+TEST INFRASTRUCTURE ONLY. Only ``tests/``, ``__graft_entry__.smoke()`` and the
+CPU-baseline leg of ``bench.py`` may import this package. The HIP training
+path (``paper_2606_30497_amd``) never imports it, and this package never
+imports that one; the two share no code. Both consume arrays from the
+``datagen`` module, which holds no training arithmetic.
+
+The arithmetic lives in ``oracle.c`` (plain fp64 loops, paper Sec. II.A
+eqs. (1)-(9) and Sec. III eqs. (11)-(19)); this file only marshals numpy
+arrays into it.
+
+Pins (tests/test_oracle_pins.py): central finite differences, the closed form
+of an all-active (linear) net, a hand-worked two-sample step, the strict
+ReLU'(0) = 0 convention, torch float64 autograd at the real shapes, and
+invariants of the batch-size scaling.
+"""
+from __future__ import annotations
+
+import ctypes
+import os
+import subprocess
+
+import numpy as np
+
+_HERE = os.path.dirname(os.path.abspath(__file__))
+_SRC = os.path.join(_HERE, "oracle.c")
+_LIB = os.path.join(_HERE, "liboracle.so")
+_lib = None
+
+_f32p = np.ctypeslib.ndpointer(np.float32, flags="C_CONTIGUOUS")
+_f64p = np.ctypeslib.ndpointer(np.float64, flags="C_CONTIGUOUS")
+_i32p = np.ctypeslib.ndpointer(np.int32, flags="C_CONTIGUOUS")
+
+
+def build(force: bool = True) -> str:
+    """Compile liboracle.so with gcc (plain -O2, no FMA contraction, no fast-math)."""
+    if force or not os.path.exists(_LIB):
+        tmp = _LIB + ".tmp%d" % os.getpid()
+        subprocess.check_call(["gcc", "-O2", "-std=c11", "-fPIC", "-shared",
+                               "-ffp-contract=off", "-fno-fast-math", "-Wall",
+                               "-o", tmp, _SRC, "-lm"])
+        os.replace(tmp, _LIB)
+    return _LIB
+
+
+def _load():
+    global _lib
+    if _lib is None:
+        if not os.path.exists(_LIB):
+            build()
+        lib = ctypes.CDLL(_LIB)
+        lib.oracle_forward.restype = ctypes.c_int
+        lib.oracle_forward.argtypes = [_f32p, ctypes.c_int64, ctypes.c_void_p, ctypes.c_int64,
+                                       ctypes.c_int32, ctypes.c_int32, _f64p, _f64p, _f64p]
+        lib.oracle_grad.restype = ctypes.c_int
+        lib.oracle_grad.argtypes = [_f32p, _f32p, ctypes.c_int64, ctypes.c_void_p, ctypes.c_int64,
+                                    ctypes.c_int32, ctypes.c_int32, _f64p, _f64p, _f64p, _f64p,
+                                    ctypes.POINTER(ctypes.c_double), ctypes.c_void_p,
+                                    ctypes.c_void_p]
+        lib.oracle_train.restype = ctypes.c_int
+        lib.oracle_train.argtypes = [_f32p, _f32p, ctypes.c_int64, ctypes.c_int32, ctypes.c_int32,
+                                     _f64p, _f64p, ctypes.c_int64, ctypes.c_double,
+                                     ctypes.c_int32, ctypes.c_void_p, ctypes.c_int64,
+                                     ctypes.c_void_p, ctypes.c_void_p,
+                                     ctypes.POINTER(ctypes.c_int64)]
+        _lib = lib
+    return _lib
+
+
+def _ptr(a):
+    return None if a is None else a.ctypes.data_as(ctypes.c_void_p)
+
+
+def _idx(idx):
+    return None if idx is None else np.ascontiguousarray(idx, dtype=np.int32)
+
+
+def forward(X, W1, W2, idx=None, nb=None):
+    """Ypred (fp64) for rows ``idx`` of X (all rows when idx is None)."""
+    X = np.ascontiguousarray(X, dtype=np.float32)
+    W1 = np.ascontiguousarray(W1, dtype=np.float64)
+    W2 = np.ascontiguousarray(np.reshape(W2, -1), dtype=np.float64)
+    idx = _idx(idx)
+    d, h = W1.shape
+    if nb is None:
+        nb = X.shape[0] if idx is None else idx.shape[0]
+    out = np.empty(nb, dtype=np.float64)
+    rc = _load().oracle_forward(X, X.shape[0], _ptr(idx), nb, d, h, W1, W2, out)
+    if rc != 0:
+        raise ValueError("oracle_forward failed: %d" % rc)
+    return out
+
+
+def grad(X, Y, W1, W2, idx=None, nb=None, want_z=False):
+    """Gradients of the batch MSE: returns (dW1 [d,h], dW2 [h], loss[, z, zabs])."""
+    X = np.ascontiguousarray(X, dtype=np.float32)
+    Y = np.ascontiguousarray(np.reshape(Y, -1), dtype=np.float32)
+    W1 = np.ascontiguousarray(W1, dtype=np.float64)
+    W2 = np.ascontiguousarray(np.reshape(W2, -1), dtype=np.float64)
+    idx = _idx(idx)
+    d, h = W1.shape
+    if nb is None:
+        nb = X.shape[0] if idx is None else idx.shape[0]
+    dW1 = np.empty((d, h), dtype=np.float64)
+    dW2 = np.empty(h, dtype=np.float64)
+    loss = ctypes.c_double(0.0)
+    z = zabs = None
+    if want_z:
+        z = np.empty((nb, h), dtype=np.float64)
+        zabs = np.empty((nb, h), dtype=np.float64)
+    rc = _load().oracle_grad(X, Y, X.shape[0], _ptr(idx), nb, d, h, W1, W2, dW1, dW2,
+                             ctypes.byref(loss), _ptr(z), _ptr(zabs))
+    if rc != 0:
+        raise ValueError("oracle_grad failed: %d" % rc)
+    if want_z:
+        return dW1, dW2, loss.value, z, zabs
+    return dW1, dW2, loss.value
+
+
+def train(X, Y, W1, W2, batch, lr, epochs, perm=None, max_steps=-1):
+    """Mini-batch SGD in fp64. Returns dict(W1, W2, step_loss, epoch_loss, steps)."""
+    X = np.ascontiguousarray(X, dtype=np.float32)
+    Y = np.ascontiguousarray(np.reshape(Y, -1), dtype=np.float32)
+    W1 = np.array(W1, dtype=np.float64, order="C", copy=True)
+    W2 = np.array(np.reshape(W2, -1), dtype=np.float64, copy=True)
+    n = X.shape[0]
+    d, h = W1.shape
+    if perm is not None:
+        perm = np.ascontiguousarray(perm, dtype=np.int32)
+        if perm.shape != (epochs, n):
+            raise ValueError("perm must be [epochs, n]")
+    spe = -(-n // batch)
+    total = spe * epochs if max_steps < 0 else min(max_steps, spe * epochs)
+    step_loss = np.zeros(max(total, 1), dtype=np.float64)
+    epoch_loss = np.zeros(max(epochs, 1), dtype=np.float64)
+    steps = ctypes.c_int64(0)
+    rc = _load().oracle_train(X, Y, n, d, h, W1, W2, batch, float(lr), epochs, _ptr(perm),
+                              max_steps, _ptr(step_loss), _ptr(epoch_loss), ctypes.byref(steps))
+    if rc != 0:
+        raise ValueError("oracle_train failed: %d" % rc)
+    return dict(W1=W1, W2=W2, step_loss=step_loss[:steps.value],
+                epoch_loss=epoch_loss[:epochs], steps=steps.value)
+
+
+class swapped_library:
+    """Context manager that points this module at another build of oracle.c.
+
+    Used only by the mutation tests, which compile deliberately broken copies
+    of the oracle and check that the pins reject each of them."""
+
+    def __init__(self, path):
+        self.path = path
+        self.saved = None
+
+    def __enter__(self):
+        global _lib, _LIB
+        self.saved = (_lib, _LIB)
+        _lib, _LIB = None, self.path
+        _load()
+        return self
+
+    def __exit__(self, *exc):
+        global _lib, _LIB
+        _lib, _LIB = self.saved
+        return False
