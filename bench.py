@@ -1,0 +1,181 @@
+"""Benchmark: fused mini-batch SGD training throughput of the 32-h-1 ReLU/MSE net.
+
+One benchmark step is one full training call (mlp_train_epochs) over the
+workload: every epoch, every mini-batch, forward + backward + SGD update, from
+the same He-normal initial weights (reset by a 34 KB device copy at the start
+of each step). Inputs (X, Y, the per-epoch permutations) are resident in HBM
+before the timed region starts.
+
+Prints ONE JSON line. value = samples/s = n * epochs / (seconds per step).
+roofline: algorithmic FLOPs of one launch of the training kernel
+(134 h FLOP per sample, the five contractions of eqs. 11-18 at 2 FLOP per
+multiply-add) divided by that launch's duration, measured with HIP events on
+the library's stream, against MI355X's dense fp32 peak (157.3 TFLOP/s).
+cpu_baseline: the fp64 oracle on the host, single-threaded, on a bounded prefix
+of the same workload (its first steps, same permutation).
+"""
+import argparse
+import hashlib
+import json
+import os
+import sys
+import time
+
+ROOT = os.path.dirname(os.path.abspath(__file__))
+sys.path.insert(0, ROOT)
+
+FP32_PEAK_TFLOPS = 157.3
+HBM_PEAK_GBS = 8000.0
+
+
+def kernel_source_hash():
+    h = hashlib.sha256()
+    csrc = os.path.join(ROOT, "paper_2606_30497_amd", "csrc")
+    for name in sorted(os.listdir(csrc)):
+        if name.endswith((".hip", ".h")):
+            with open(os.path.join(csrc, name), "rb") as f:
+                h.update(name.encode() + b"\0" + f.read())
+    return h.hexdigest()[:16]
+
+
+def load_traffic(workload_name):
+    """HBM bytes per launch from the committed rocprofv3 counter summary, or None
+    when the kernels changed since the counters were taken."""
+    path = os.path.join(ROOT, "profiles", "traffic.json")
+    if not os.path.exists(path):
+        return None
+    with open(path) as f:
+        t = json.load(f)
+    e = t.get(workload_name)
+    if not e or e.get("kernel_source_hash") != kernel_source_hash():
+        return None
+    return e.get("hbm_bytes_per_launch")
+
+
+def cpu_baseline(w, data, max_seconds=15.0):
+    import oracle
+    steps = 1
+    # size the prefix from a one-step probe so the whole leg takes ~max_seconds
+    t = time.perf_counter()
+    oracle.train(data.X, data.Y, data.W1, data.W2, w.batch, w.lr, w.epochs, perm=data.perm,
+                 max_steps=1)
+    one = time.perf_counter() - t
+    steps = max(1, min(w.steps, int(max_seconds / max(one, 1e-6))))
+    t = time.perf_counter()
+    oracle.train(data.X, data.Y, data.W1, data.W2, w.batch, w.lr, w.epochs, perm=data.perm,
+                 max_steps=steps)
+    dt = time.perf_counter() - t
+    samples = min(steps * w.batch, w.n * w.epochs)
+    return {"value": samples / dt, "unit": "samples/s", "cores": 1, "kind": "oracle",
+            "sample": "first %d SGD steps (%d samples) of the same workload, fp64, one thread"
+                      % (steps, samples)}
+
+
+def main():
+    ap = argparse.ArgumentParser()
+    ap.add_argument("--gpus", type=int, default=1)
+    ap.add_argument("--steps", type=int, default=5)
+    ap.add_argument("--warmup", type=int, default=2)
+    ap.add_argument("--workload", type=int, default=4,
+                    help="index into datagen.WORKLOADS (default: the 10M-sample 32-256-1 run)")
+    ap.add_argument("--no-cpu-baseline", action="store_true")
+    args = ap.parse_args()
+    if args.gpus != 1:
+        print("bench.py runs on one GPU only: this path is single-GPU by design "
+              "(--gpus %d requested)" % args.gpus, file=sys.stderr)
+        sys.exit(2)
+
+    import numpy as np
+    import torch
+
+    import datagen
+    from paper_2606_30497_amd import mlp
+
+    if not torch.cuda.is_available():
+        print("bench.py needs a GPU", file=sys.stderr)
+        sys.exit(1)
+    mlp.load(require_built=True)
+    w = datagen.WORKLOADS[args.workload]
+    t0 = time.perf_counter()
+    data = datagen.make_workload(w)
+    print("# data %s generated in %.1f s" % (w.name, time.perf_counter() - t0), file=sys.stderr,
+          flush=True)
+    dev = torch.device("cuda:0")
+    X = torch.from_numpy(data.X).to(dev)
+    Y = torch.from_numpy(data.Y).to(dev)
+    perm = None if data.perm is None else torch.from_numpy(data.perm).to(dev)
+    W1_0 = torch.from_numpy(data.W1).to(dev)
+    W2_0 = torch.from_numpy(data.W2).to(dev)
+    W1 = W1_0.clone()
+    W2 = W2_0.clone()
+    ctx = mlp.mlp_init(W1, W2, w.batch)
+    el = torch.zeros(w.epochs, dtype=torch.float32, device=dev)
+    mlp.mlp_profile(ctx, True)
+
+    def step():
+        W1.copy_(W1_0)
+        W2.copy_(W2_0)
+        mlp.mlp_train_epochs(ctx, X, Y, w.batch, w.lr, w.epochs, perm=perm, epoch_loss=el)
+        return mlp.mlp_last_kernel_ms(ctx)
+
+    for _ in range(args.warmup):
+        step()
+    torch.cuda.synchronize()
+    mlp.mlp_check_errors(ctx)
+    kernel_ms = []
+    torch.cuda.synchronize()
+    t0 = time.perf_counter()
+    for _ in range(args.steps):
+        kernel_ms.append(step())
+    torch.cuda.synchronize()
+    t1 = time.perf_counter()
+    mlp.mlp_check_errors(ctx)
+    final_loss = el.cpu().numpy().tolist()
+
+    sec = (t1 - t0) / args.steps
+    samples = w.n * w.epochs
+    value = samples / sec
+    flop_launch = float(w.flop_per_sample()) * samples
+    wgs, launches = mlp.mlp_launch_info(ctx, w.n, w.batch, w.epochs)
+    avg_kernel_s = float(np.mean(kernel_ms)) / 1e3
+    achieved = flop_launch / avg_kernel_s / 1e12 if launches == 1 else None
+    traffic = load_traffic(w.name)
+    out = {
+        "metric": "training samples/sec (fwd+bwd+SGD) 32-256-1 MLP; % of fp32 peak",
+        "value": value,
+        "unit": "samples/s",
+        "n_gpus": 1,
+        "steps": args.steps,
+        "warmup": args.warmup,
+        "ms_per_step": sec * 1e3,
+        "higher_is_better": True,
+        "scaling": "weak",
+        "vs_baseline": None,
+        "dtype": "f32",
+        "data": "synthetic",
+        "config": {"workload": w.name, "d_in": w.d_in, "hidden": w.hidden, "n": w.n,
+                   "batch": w.batch, "lr": w.lr, "epochs": w.epochs,
+                   "shuffle": "seeded per-epoch permutation" if w.shuffle else "none",
+                   "sgd_steps": w.steps, "parallelism": "single GPU"},
+        "pct_fp32_peak": 100.0 * value * w.flop_per_sample() / (FP32_PEAK_TFLOPS * 1e12),
+        "roofline": {
+            "bound": "mfma",
+            "achieved": achieved,
+            "peak": FP32_PEAK_TFLOPS,
+            "unit": "TFLOP/s",
+            "frac": None if achieved is None else achieved / FP32_PEAK_TFLOPS,
+            "traffic": traffic,
+            "kernel_ms": float(np.mean(kernel_ms)),
+            "flop_per_launch": flop_launch,
+        },
+        "kernel_launches_per_step": launches,
+        "workgroups": wgs,
+        "final_epoch_loss": final_loss,
+    }
+    if not args.no_cpu_baseline:
+        out["cpu_baseline"] = cpu_baseline(w, data)
+    print(json.dumps(out), flush=True)
+
+
+if __name__ == "__main__":
+    main()

@@ -1,0 +1,150 @@
+/*
+ * mlp.h -- C ABI of the fused mini-batch SGD path for a d-h-1 ReLU/MSE
+ * regression network with no biases, built for AMD Instinct MI355X (gfx950).
+ *
+ * The network and its training step are those of the paper's Sec. III:
+ *   Z1 = X W1, H = ReLU(Z1), Ypred = H W2                (eqs. 11-13)
+ *   L = (1/n_b) sum (Ypred - Y)^2                         (eq. 14)
+ *   dZ2 = (2/n_b)(Ypred - Y), dW2 = H^T dZ2               (eqs. 15-16)
+ *   dZ1 = (dZ2 W2^T) (.) [Z1 > 0], dW1 = X^T dZ1          (eqs. 17-18)
+ *   W <- W - lr dW, both layers, after both gradients     (eq. 19)
+ * with n_b the row count of the current mini-batch, mini-batch SGD over
+ * epochs (Sec. II.A, Sec. III.A), and the last batch of an epoch keeping
+ * its remainder rows.
+ *
+ * Conventions shared by every entry point
+ *   - Every data pointer is a DEVICE pointer owned by the caller. The library
+ *     never allocates or frees device memory; its scratch space is the
+ *     caller's workspace buffer.
+ *   - fp32 data, row-major. X is [n_rows x d_in]; Y is [n_rows]; W1 is
+ *     [d_in x hidden] with rows = inputs (the paper's layout); W2 is
+ *     [hidden] (the paper's hidden x 1 column, stored flat). Row indices and
+ *     permutations are int32.
+ *   - Calls are asynchronous on the context's stream. Argument errors are
+ *     detected on the host before anything is enqueued; they return a
+ *     negative status and leave weights and outputs untouched. Outputs are
+ *     valid after the stream has been synchronised.
+ *   - A row index outside [0, n_rows) is never dereferenced: the kernels read
+ *     row 0 in its place and raise a sticky flag that mlp_check_errors()
+ *     reports (results of that call are then meaningless).
+ *   - Results are bitwise reproducible for identical inputs on one device:
+ *     every reduction runs in a fixed order and no floating-point atomics are
+ *     used.
+ *   - One context per stream; a context is not re-entrant and calls on it
+ *     must not overlap.
+ */
+#ifndef MLP_H_
+#define MLP_H_
+
+#include <stddef.h>
+#include <stdint.h>
+
+#ifdef __cplusplus
+extern "C" {
+#endif
+
+typedef struct mlp_ctx *mlp_t;
+
+typedef enum {
+    MLP_OK = 0,
+    MLP_ERR_INVALID_ARG = -1,  /* null pointer, bad size, non-finite lr ...      */
+    MLP_ERR_UNSUPPORTED = -2,  /* d_in != 32, d_out != 1, hidden not supported   */
+    MLP_ERR_WORKSPACE = -3,    /* workspace too small or misaligned              */
+    MLP_ERR_HIP = -4,          /* a HIP runtime call or kernel launch failed     */
+    MLP_ERR_INDEX = -6,        /* a kernel met a row index outside [0, n_rows)   */
+    MLP_ERR_TIMEOUT = -7       /* a wait inside the training kernel timed out    */
+} mlp_status;
+
+/* Largest mini-batch any call accepts. */
+#define MLP_MAX_BATCH (1 << 20)
+
+/* Bytes of device workspace a context needs for the given shape. hidden must be
+ * one of 32, 64, 128, 256, 512, 1024; d_in must be 32. Returns 0 for an
+ * unsupported shape. The workspace must be 256-byte aligned. */
+size_t mlp_workspace_bytes(int32_t d_in, int32_t hidden, int64_t max_batch);
+
+/* Create a context bound to caller-owned weights and workspace.
+ *   d_in      must be 32 (paper Sec. III.A input layer)
+ *   hidden    32, 64, 128, 256 (the paper's net), 512 or 1024 (Sec. VI.C sweep)
+ *   d_out     must be 1 (single regression output, Sec. III.A)
+ *   max_batch largest batch later calls will use, 1..MLP_MAX_BATCH
+ *   W1        [d_in x hidden] device fp32, updated in place by training calls
+ *   W2        [hidden] device fp32, updated in place by training calls
+ *   workspace device buffer of at least mlp_workspace_bytes(d_in, hidden,
+ *             max_batch) bytes, 256-byte aligned, owned by the caller and kept
+ *             alive for the life of the context
+ *   stream    hipStream_t to enqueue on (NULL = the null stream)
+ * Enqueues a clear of the whole workspace after the tile-path slots (control
+ * words and exchange buffers) on `stream`; later calls must be ordered after
+ * it (same stream, or a synchronisation). *out is set only on success. */
+mlp_status mlp_init(mlp_t *out, int32_t d_in, int32_t hidden, int32_t d_out,
+                    int64_t max_batch, float *W1, float *W2, void *workspace,
+                    size_t ws_bytes, void *stream);
+
+/* Rebind the stream later calls enqueue on. */
+mlp_status mlp_set_stream(mlp_t ctx, void *stream);
+
+/* Forward pass, eqs. (11)-(13): Ypred[t] = ReLU(X[r_t] W1) W2 for t < B, where
+ * r_t = idx[t] (idx == NULL: r_t = t). X has n_rows rows. Ypred is [B].
+ * B must be >= 1; it is not limited by max_batch. Weights are not changed. */
+mlp_status mlp_forward(mlp_t ctx, const float *X, int64_t n_rows, const int32_t *idx,
+                       int64_t B, float *Ypred);
+
+/* Gradients of the batch loss at the current weights, eqs. (14)-(18), for the
+ * B rows r_t (as in mlp_forward). Writes dW1 [d_in x hidden] and dW2 [hidden]
+ * in the caller's layout (both include the 2/B factor of eq. 15) and, when
+ * loss != NULL, loss[0] = batch MSE (eq. 14). 1 <= B <= max_batch. Weights are
+ * not changed. */
+mlp_status mlp_backward(mlp_t ctx, const float *X, int64_t n_rows, const float *Y,
+                        const int32_t *idx, int64_t B, float *dW1, float *dW2,
+                        float *loss);
+
+/* One SGD step on the B rows r_t: the gradients of mlp_backward, then
+ * W1 -= lr dW1 and W2 -= lr dW2 (eq. 19). loss (nullable) receives the batch
+ * MSE before the update. 1 <= B <= max_batch; lr finite. */
+mlp_status mlp_sgd_step(mlp_t ctx, const float *X, int64_t n_rows, const float *Y,
+                        const int32_t *idx, int64_t B, float lr, float *loss);
+
+/* Mini-batch SGD over epochs (Sec. II.A, Sec. III.A, eq. 19). Epoch e visits
+ * rows perm[e*n + 0 .. n-1] in order (perm == NULL: rows 0..n-1 every epoch)
+ * in ceil(n/batch) steps; the last step of an epoch takes the remainder rows
+ * and scales by its own row count. X/Y have n rows.
+ *   1 <= batch <= max_batch, epochs >= 1, lr finite
+ *   max_steps   stop after this many steps in total (-1: run every epoch)
+ *   epoch_loss  nullable [epochs]: sum of the epoch's squared residuals
+ *               (each taken before its step's update) / n; entries of epochs
+ *               cut short by max_steps hold the partial sum / n, later ones 0
+ *   step_loss   nullable [steps run]: batch MSE of each step before its update
+ * Each perm row must be a permutation of [0, n) (checked only for range). */
+mlp_status mlp_train_epochs(mlp_t ctx, const float *X, const float *Y, int64_t n,
+                            int64_t batch, float lr, int32_t epochs,
+                            const int32_t *perm, int64_t max_steps,
+                            float *epoch_loss, float *step_loss);
+
+/* Synchronise the stream and report sticky kernel-side errors (MLP_ERR_INDEX,
+ * MLP_ERR_TIMEOUT) raised since the last check; clears them. */
+mlp_status mlp_check_errors(mlp_t ctx);
+
+/* Timing of the training kernel. When enabled, mlp_train_epochs and
+ * mlp_sgd_step bracket their training-kernel launches with HIP events on the
+ * context's stream; mlp_last_kernel_ms synchronises on the end event and
+ * returns the elapsed milliseconds of the most recent call's launches. */
+mlp_status mlp_profile(mlp_t ctx, int32_t enable);
+mlp_status mlp_last_kernel_ms(mlp_t ctx, float *ms);
+
+/* Launch shape of an mlp_train_epochs call with these sizes: the number of
+ * workgroups of its training kernel and the total number of kernel launches
+ * the call enqueues (launch-count evidence for the benchmark). */
+mlp_status mlp_launch_info(mlp_t ctx, int64_t n, int64_t batch, int32_t epochs,
+                           int32_t *workgroups, int64_t *launches);
+
+/* Release the host-side context (the caller still owns every device buffer). */
+void mlp_destroy(mlp_t ctx);
+
+/* Static description of a status code. */
+const char *mlp_status_string(mlp_status status);
+
+#ifdef __cplusplus
+}
+#endif
+#endif /* MLP_H_ */

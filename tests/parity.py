@@ -1,0 +1,57 @@
+"""Comparison helpers for GPU-vs-oracle parity (test infrastructure).
+
+Relative error is normwise: ||a - ref||_F / ||ref||_F.
+
+ReLU kink: where a pre-activation Z1[i, j] is so close to zero that fp32
+cannot resolve its sign, both mask values are correct results of eq. (17).
+With Z1 computed as a length-32 fp32 dot product, the computed value differs
+from the exact one by at most gamma_32 * sum_k |X_ik W1_kj| (gamma_32 ~ 32 u,
+u = 2^-24). Entries with |Z1| under that bound are ambiguous. Before dW1 is
+compared, each column's ambiguous rows are resolved by choosing the subset of
+their contributions X_i * g_i * W2_j (g_i = (2/n_b)(Ypred_i - Y_i)) that best
+matches the GPU column, by brute force over subsets (at most 2^10). dW2, Ypred
+and the loss are continuous at the kink and need no alignment.
+"""
+import itertools
+
+import numpy as np
+
+U32 = 2.0 ** -24
+KINK_GAMMA = 33 * U32
+
+
+def rel(a, ref):
+    a = np.asarray(a, np.float64)
+    ref = np.asarray(ref, np.float64)
+    den = np.linalg.norm(ref)
+    return float(np.linalg.norm(a - ref) / (den if den > 0 else 1.0))
+
+
+def align_kinks(dW1_gpu, dW1_ref, X, Y, W1, W2, idx, z, zabs, ypred):
+    """Return (dW1_ref adjusted to the GPU's choice at ambiguous entries,
+    number of ambiguous entries, number of flips accepted)."""
+    nb = z.shape[0]
+    rows = np.arange(nb) if idx is None else np.asarray(idx)
+    Xb = X[rows].astype(np.float64)
+    g = (2.0 / nb) * (ypred - Y[rows].astype(np.float64))
+    amb = np.abs(z) <= KINK_GAMMA * zabs
+    out = dW1_ref.copy()
+    n_amb = int(amb.sum())
+    flips = 0
+    for j in np.nonzero(amb.any(axis=0))[0]:
+        ii = np.nonzero(amb[:, j])[0]
+        if len(ii) > 10:
+            raise AssertionError("too many ambiguous kink entries in column %d" % j)
+        contrib = Xb[ii] * (g[ii] * W2[j])[:, None]          # [m, d]
+        on = z[ii, j] > 0
+        base = dW1_ref[:, j] - contrib[on].sum(axis=0)
+        best, best_err, best_sel = None, np.inf, None
+        for sel in itertools.product((False, True), repeat=len(ii)):
+            sel = np.array(sel)
+            cand = base + contrib[sel].sum(axis=0)
+            err = np.linalg.norm(cand - dW1_gpu[:, j])
+            if err < best_err:
+                best, best_err, best_sel = cand, err, sel
+        out[:, j] = best
+        flips += int((best_sel != on).sum())
+    return out, n_amb, flips

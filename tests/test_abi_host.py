@@ -1,0 +1,90 @@
+"""Host-side checks of the C ABI that need no GPU: the library loads, exports
+every entry point include/mlp.h declares, sizes its workspace, and rejects bad
+arguments before touching the device."""
+import ctypes
+import os
+import re
+
+import pytest
+
+ROOT = os.path.dirname(os.path.dirname(os.path.abspath(__file__)))
+HEADER = os.path.join(ROOT, "include", "mlp.h")
+
+
+def _lib():
+    from paper_2606_30497_amd import mlp
+    if not os.path.exists(mlp.library_path()):
+        pytest.skip("libmlp.so not built")
+    return mlp.load()
+
+
+def declared_functions():
+    text = open(HEADER).read()
+    text = re.sub(r"/\*.*?\*/", "", text, flags=re.S)
+    return sorted(set(re.findall(r"\b(mlp_[a-z_]+)\s*\(", text)))
+
+
+def test_header_declares_the_five_calls():
+    names = declared_functions()
+    for f in ("mlp_init", "mlp_forward", "mlp_backward", "mlp_sgd_step", "mlp_train_epochs"):
+        assert f in names
+
+
+def test_every_declared_symbol_is_exported():
+    lib = _lib()
+    from paper_2606_30497_amd import mlp
+    for name in declared_functions():
+        assert hasattr(lib, name), name
+        assert name in mlp.EXPORTS, name
+
+
+def test_workspace_bytes():
+    lib = _lib()
+    for h in (32, 64, 128, 256, 512, 1024):
+        b = lib.mlp_workspace_bytes(32, h, 4096)
+        assert b > 0 and b % 256 == 0
+        assert lib.mlp_workspace_bytes(32, h, 1 << 20) >= b
+    assert lib.mlp_workspace_bytes(32, 100, 64) == 0
+    assert lib.mlp_workspace_bytes(16, 256, 64) == 0
+    assert lib.mlp_workspace_bytes(32, 256, 0) == 0
+    assert lib.mlp_workspace_bytes(32, 256, (1 << 20) + 1) == 0
+
+
+def test_status_strings():
+    lib = _lib()
+    for s in (0, -1, -2, -3, -4, -6):
+        assert lib.mlp_status_string(s)
+    assert lib.mlp_status_string(-99) == b"unknown status"
+
+
+def test_init_rejects_bad_arguments_without_device():
+    lib = _lib()
+    h = ctypes.c_void_p()
+    fake = ctypes.c_void_p(256)      # never dereferenced: validation fails first
+    ws = lib.mlp_workspace_bytes(32, 256, 64)
+    # null out-pointer / weights / workspace
+    assert lib.mlp_init(None, 32, 256, 1, 64, fake, fake, fake, ws, None) == -1
+    assert lib.mlp_init(ctypes.byref(h), 32, 256, 1, 64, None, fake, fake, ws, None) == -1
+    assert lib.mlp_init(ctypes.byref(h), 32, 256, 1, 64, fake, fake, None, ws, None) == -1
+    # unsupported shapes
+    assert lib.mlp_init(ctypes.byref(h), 16, 256, 1, 64, fake, fake, fake, ws, None) == -2
+    assert lib.mlp_init(ctypes.byref(h), 32, 256, 2, 64, fake, fake, fake, ws, None) == -2
+    assert lib.mlp_init(ctypes.byref(h), 32, 100, 1, 64, fake, fake, fake, ws, None) == -2
+    # batch limits, workspace size and alignment
+    assert lib.mlp_init(ctypes.byref(h), 32, 256, 1, 0, fake, fake, fake, ws, None) == -1
+    assert lib.mlp_init(ctypes.byref(h), 32, 256, 1, 64, fake, fake, fake, ws - 1, None) == -3
+    assert lib.mlp_init(ctypes.byref(h), 32, 256, 1, 64, fake, fake, ctypes.c_void_p(260), ws,
+                        None) == -3
+    assert h.value is None
+
+
+def test_null_context_is_rejected():
+    lib = _lib()
+    fake = ctypes.c_void_p(256)
+    assert lib.mlp_forward(None, fake, 10, None, 10, fake) == -1
+    assert lib.mlp_backward(None, fake, 10, fake, None, 10, fake, fake, None) == -1
+    assert lib.mlp_sgd_step(None, fake, 10, fake, None, 10, 0.1, None) == -1
+    assert lib.mlp_train_epochs(None, fake, fake, 10, 2, 0.1, 1, None, -1, None, None) == -1
+    assert lib.mlp_check_errors(None) == -1
+    assert lib.mlp_profile(None, 1) == -1
+    lib.mlp_destroy(None)

@@ -1,0 +1,389 @@
+"""GPU parity: the HIP path (through the C ABI) against the fp64 oracle.
+
+Tolerances (normwise relative error unless stated):
+  - per-step gradients dW1, dW2: <= 1e-4, after ReLU-kink alignment of dW1;
+  - batch loss and forward outputs: <= 1e-5;
+  - weights and per-step losses after 10 SGD steps: <= 1e-3. The weight change
+    W10 - W0 is also held to 1e-3, which is the meaningful check since
+    lr * dW is small against W. The 32-1024-1 workload at lr 0.005 is the
+    exception: its first steps are a divergent transient (the loss grows by
+    about five orders of magnitude), and its 10-step map amplifies a relative
+    perturbation of 1e-6 in W0 to about 1.4e-3 in W1 (measured with the oracle
+    alone), so no fp32 implementation can meet 1e-3 there; its W1 bar is 1e-2.
+"""
+import numpy as np
+import pytest
+import torch
+
+import datagen
+import oracle
+from tests.parity import align_kinks, rel
+
+pytestmark = pytest.mark.gpu
+
+H_ALL = (32, 64, 128, 256, 512, 1024)
+
+
+@pytest.fixture(scope="module")
+def mlp():
+    assert torch.cuda.is_available(), "GPU tests need a GPU"
+    from paper_2606_30497_amd import mlp as m
+    m.load(require_built=True)
+    return m
+
+
+def _to(a, dtype=None):
+    t = torch.from_numpy(np.ascontiguousarray(a))
+    if dtype is not None:
+        t = t.to(dtype)
+    return t.cuda()
+
+
+def _ctx(mlp, W1, W2, max_batch):
+    w1 = _to(W1.astype(np.float32))
+    w2 = _to(np.reshape(W2, -1).astype(np.float32))
+    return mlp.mlp_init(w1, w2, max_batch), w1, w2
+
+
+def _rows(rng, n, B):
+    return rng.integers(0, n, size=B).astype(np.int32)
+
+
+# --- forward -------------------------------------------------------------------
+
+@pytest.mark.parametrize("h", H_ALL)
+def test_forward_matches_oracle(mlp, h):
+    rng = np.random.default_rng(h)
+    d = datagen.make_data(3001, h, seed=100 + h, with_perm=False)
+    ctx, _, _ = _ctx(mlp, d.W1, d.W2, 64)
+    X = _to(d.X)
+    idx = _rows(rng, 3001, 2777)
+    yp = mlp.mlp_forward(ctx, X, _to(idx)).cpu().numpy()
+    ref = oracle.forward(d.X, d.W1, d.W2, idx=idx)
+    assert rel(yp, ref) < 1e-5
+    yp_all = mlp.mlp_forward(ctx, X).cpu().numpy()
+    assert rel(yp_all, oracle.forward(d.X, d.W1, d.W2)) < 1e-5
+    mlp.mlp_check_errors(ctx)
+
+
+# --- per-step gradients ----------------------------------------------------------
+
+def _check_grad(mlp, h, B, n=5000, seed=0, idx_none=False):
+    rng = np.random.default_rng(seed)
+    d = datagen.make_data(n, h, seed=200 + h + B, with_perm=False)
+    ctx, _, _ = _ctx(mlp, d.W1, d.W2, max(B, 1))
+    idx = None if idx_none else _rows(rng, n, B)
+    dW1, dW2, loss = mlp.mlp_backward(ctx, _to(d.X), _to(d.Y), None if idx is None else _to(idx),
+                                      B=B)
+    torch.cuda.synchronize()
+    mlp.mlp_check_errors(ctx)
+    g1, g2, gl = dW1.cpu().numpy(), dW2.cpu().numpy(), float(loss.cpu()[0])
+    W1, W2 = d.W1.astype(np.float64), d.W2.astype(np.float64)
+    r1, r2, rL, z, zabs = oracle.grad(d.X, d.Y, W1, W2, idx=idx, nb=B, want_z=True)
+    yp = oracle.forward(d.X, W1, W2, idx=idx, nb=B)
+    r1a, n_amb, flips = align_kinks(g1, r1, d.X, d.Y, W1, W2, idx, z, zabs, yp)
+    e1, e2 = rel(g1, r1a), rel(g2, r2)
+    assert e1 <= 1e-4, (e1, n_amb, flips)
+    assert e2 <= 1e-4, e2
+    assert abs(gl - rL) <= 1e-5 * rL
+    return e1, e2
+
+
+@pytest.mark.parametrize("h", H_ALL)
+@pytest.mark.parametrize("B", [1, 7, 64, 160, 1000])
+def test_backward_small_batches(mlp, h, B):
+    _check_grad(mlp, h, B, seed=B)
+
+
+@pytest.mark.parametrize("h,B", [(256, 4096), (256, 1664), (256, 576), (1024, 1024),
+                                 (1024, 576), (256, 256), (256, 64)])
+def test_backward_workload_batches(mlp, h, B):
+    _check_grad(mlp, h, B, n=20000, seed=B)
+
+
+def test_backward_identity_rows(mlp):
+    _check_grad(mlp, 256, 333, n=333, idx_none=True)
+
+
+# --- worked examples embedded in 32-h-1 by zero padding ---------------------------
+
+def _embed(X, W1, W2, h):
+    Xp = np.zeros((X.shape[0], 32), np.float32)
+    Xp[:, :X.shape[1]] = X
+    W1p = np.zeros((32, h), np.float32)
+    W1p[:W1.shape[0], :W1.shape[1]] = W1
+    W2p = np.zeros(h, np.float32)
+    W2p[:W2.shape[0]] = W2
+    return Xp, W1p, W2p
+
+
+@pytest.mark.parametrize("h", [32, 256, 1024])
+def test_worked_two_sample_step_embedded(mlp, h):
+    import json, os
+    g = json.load(open(os.path.join(os.path.dirname(__file__), "golden", "worked_two_sample.json")))
+    X, W1, W2 = _embed(np.array(g["X"], np.float32), np.array(g["W1"]), np.array(g["W2"]), h)
+    Y = np.array(g["Y"], np.float32)
+    ctx, w1, w2 = _ctx(mlp, W1, W2, 2)
+    dW1, dW2, loss = mlp.mlp_backward(ctx, _to(X), _to(Y))
+    dW1, dW2 = dW1.cpu().numpy(), dW2.cpu().numpy()
+    exp1 = np.zeros((32, h)); exp1[:2, :2] = g["dW1"]
+    exp2 = np.zeros(h); exp2[:2] = g["dW2"]
+    assert np.array_equal(dW1, exp1) and np.array_equal(dW2, exp2)
+    assert float(loss.cpu()[0]) == g["loss"]
+    mlp.mlp_sgd_step(ctx, _to(X), _to(Y), g["lr"])
+    np.testing.assert_allclose(w1.cpu().numpy()[:2, :2], g["W1_next"], atol=1e-6)
+    np.testing.assert_allclose(w2.cpu().numpy()[:2], g["W2_next"], atol=1e-6)
+    assert np.all(w1.cpu().numpy()[2:, :] == 0) and np.all(w1.cpu().numpy()[:, 2:] == 0)
+    assert np.all(w2.cpu().numpy()[2:] == 0)
+
+
+def test_relu_zero_embedded(mlp):
+    import json, os
+    g = json.load(open(os.path.join(os.path.dirname(__file__), "golden", "relu_zero.json")))
+    X, W1, W2 = _embed(np.array(g["X"], np.float32), np.array(g["W1"]), np.array(g["W2"]), 256)
+    ctx, _, _ = _ctx(mlp, W1, W2, 1)
+    dW1, dW2, loss = mlp.mlp_backward(ctx, _to(X), _to(np.array(g["Y"], np.float32)))
+    assert torch.all(dW1 == 0) and torch.all(dW2 == 0)
+    assert float(loss.cpu()[0]) == g["loss"]
+
+
+# --- training ------------------------------------------------------------------
+
+_DATA = {}
+
+
+def _workload_data(k):
+    if k not in _DATA:
+        _DATA.clear()
+        w = datagen.WORKLOADS[k]
+        d = datagen.make_workload(w)
+        _DATA[k] = (w, d)
+    return _DATA[k]
+
+
+def _train_gpu(mlp, d, batch, lr, epochs, max_steps=-1, perm=None):
+    ctx, w1, w2 = _ctx(mlp, d.W1, d.W2, batch)
+    n = d.X.shape[0]
+    spe = -(-n // batch)
+    steps = spe * epochs if max_steps < 0 else min(max_steps, spe * epochs)
+    el = torch.zeros(epochs, dtype=torch.float32, device="cuda")
+    sl = torch.zeros(steps, dtype=torch.float32, device="cuda")
+    p = None if perm is None else _to(perm)
+    mlp.mlp_train_epochs(ctx, _to(d.X), _to(d.Y), batch, lr, epochs, perm=p, max_steps=max_steps,
+                         epoch_loss=el, step_loss=sl)
+    torch.cuda.synchronize()
+    mlp.mlp_check_errors(ctx)
+    return w1.cpu().numpy(), w2.cpu().numpy(), sl.cpu().numpy(), el.cpu().numpy()
+
+
+W1_BAR = {3: 1e-2}
+
+
+@pytest.mark.parametrize("k", range(5))
+def test_train_ten_steps_full_workload(mlp, k):
+    w, d = _workload_data(k)
+    print("workload", w.name, flush=True)
+    g1, g2, gsl, _ = _train_gpu(mlp, d, w.batch, w.lr, w.epochs, max_steps=10, perm=d.perm)
+    ref = oracle.train(d.X, d.Y, d.W1, d.W2, w.batch, w.lr, w.epochs, perm=d.perm, max_steps=10)
+    bar1 = W1_BAR.get(k, 1e-3)
+    assert rel(g1, ref["W1"]) <= bar1
+    assert rel(g2, ref["W2"]) <= 1e-3
+    W10 = d.W1.astype(np.float64)
+    assert rel(g1 - W10, ref["W1"] - W10) <= max(bar1, 1e-3)
+    assert rel(g2 - d.W2, ref["W2"] - d.W2.astype(np.float64)) <= 1e-3
+    assert np.all(np.abs(gsl - ref["step_loss"]) <= 1e-3 * np.abs(ref["step_loss"]))
+
+
+def test_train_epochs_with_tail_and_shuffle(mlp):
+    n, h, B, E, lr = 1000, 256, 64, 3, 0.01
+    d = datagen.make_data(n, h, epochs=E, shuffle=True, seed=77)
+    g1, g2, gsl, gel = _train_gpu(mlp, d, B, lr, E, perm=d.perm)
+    ref = oracle.train(d.X, d.Y, d.W1, d.W2, B, lr, E, perm=d.perm)
+    assert len(gsl) == ref["steps"] == 48
+    assert rel(g1 - d.W1, ref["W1"] - d.W1.astype(np.float64)) <= 1e-3
+    assert rel(g2 - d.W2, ref["W2"] - d.W2.astype(np.float64)) <= 1e-3
+    assert np.all(np.abs(gsl - ref["step_loss"]) <= 1e-3 * ref["step_loss"])
+    assert np.all(np.abs(gel - ref["epoch_loss"]) <= 1e-3 * ref["epoch_loss"])
+
+
+def test_full_first_workload_run(mlp):
+    w, d = _workload_data(0)
+    g1, g2, gsl, gel = _train_gpu(mlp, d, w.batch, w.lr, w.epochs, perm=d.perm)
+    ref = oracle.train(d.X, d.Y, d.W1, d.W2, w.batch, w.lr, w.epochs, perm=d.perm)
+    assert ref["steps"] == 80
+    assert rel(g1 - d.W1, ref["W1"] - d.W1.astype(np.float64)) <= 1e-3
+    assert np.all(np.abs(gel - ref["epoch_loss"]) <= 1e-3 * ref["epoch_loss"])
+
+
+def test_deterministic_and_prefix_consistent(mlp):
+    w, d = _workload_data(1)
+    a = _train_gpu(mlp, d, w.batch, w.lr, 2, perm=d.perm[:2].copy())
+    b = _train_gpu(mlp, d, w.batch, w.lr, 2, perm=d.perm[:2].copy())
+    for x, y in zip(a, b):
+        assert np.array_equal(x, y)
+    c = _train_gpu(mlp, d, w.batch, w.lr, 2, max_steps=10, perm=d.perm[:2].copy())
+    assert np.array_equal(c[2], a[2][:10])
+    # epoch loss is the row-weighted mean of the step losses
+    spe = w.steps_per_epoch
+    nb = np.full(spe, w.batch, np.float64)
+    nb[-1] = w.tail
+    for e in range(2):
+        exp = np.sum(a[2][e * spe:(e + 1) * spe] * nb) / w.n
+        assert abs(a[3][e] - exp) <= 1e-5 * exp
+    assert a[3][1] < a[3][0]
+
+
+def test_identity_order_when_perm_is_null(mlp):
+    w, d = _workload_data(0)
+    a = _train_gpu(mlp, d, w.batch, w.lr, 2)
+    b = _train_gpu(mlp, d, w.batch, w.lr, 2, perm=datagen.identity_perm(2, w.n))
+    for x, y in zip(a, b):
+        assert np.array_equal(x, y)
+
+
+# --- errors --------------------------------------------------------------------
+
+def test_out_of_range_row_is_flagged_not_read(mlp):
+    d = datagen.make_data(100, 256, seed=1, with_perm=False)
+    ctx, w1, _ = _ctx(mlp, d.W1, d.W2, 64)
+    idx = np.arange(64, dtype=np.int32)
+    idx[5] = 100                        # one past the end: the kernel reads row 0 instead
+    mlp.mlp_backward(ctx, _to(d.X), _to(d.Y), _to(idx))
+    with pytest.raises(mlp.MLPError) as ei:
+        mlp.mlp_check_errors(ctx)
+    assert ei.value.status == -6
+    mlp.mlp_check_errors(ctx)          # the flag is cleared by the check
+
+
+def test_host_argument_errors_leave_weights_untouched(mlp):
+    d = datagen.make_data(100, 256, seed=2, with_perm=False)
+    ctx, w1, w2 = _ctx(mlp, d.W1, d.W2, 64)
+    before = (w1.clone(), w2.clone())
+    X, Y = _to(d.X), _to(d.Y)
+    lib = mlp.load()
+    assert lib.mlp_sgd_step(ctx.handle, X.data_ptr(), 100, Y.data_ptr(), None, 65, 0.1, None) == -1
+    assert lib.mlp_sgd_step(ctx.handle, X.data_ptr(), 100, Y.data_ptr(), None, 64,
+                            float("nan"), None) == -1
+    assert lib.mlp_sgd_step(ctx.handle, X.data_ptr(), 100, Y.data_ptr(), None, 0, 0.1, None) == -1
+    assert lib.mlp_train_epochs(ctx.handle, X.data_ptr(), Y.data_ptr(), 100, 65, 0.1, 1, None, -1,
+                                None, None) == -1
+    assert lib.mlp_train_epochs(ctx.handle, X.data_ptr(), Y.data_ptr(), 100, 64, 0.1, 0, None, -1,
+                                None, None) == -1
+    assert lib.mlp_backward(ctx.handle, X.data_ptr(), 100, Y.data_ptr(), None, 101, None, None,
+                            None) == -1
+    torch.cuda.synchronize()
+    assert torch.equal(before[0], w1) and torch.equal(before[1], w2)
+
+
+# --- every plan of the persistent trainer, both paths, the coherent fallback -----
+
+import os
+import contextlib
+
+
+@contextlib.contextmanager
+def _env(**kv):
+    old = {k: os.environ.get(k) for k in kv}
+    try:
+        for k, v in kv.items():
+            if v is None:
+                os.environ.pop(k, None)
+            else:
+                os.environ[k] = str(v)
+        yield
+    finally:
+        for k, v in old.items():
+            if v is None:
+                os.environ.pop(k, None)
+            else:
+                os.environ[k] = v
+
+
+def _px_options(h):
+    return [px for px in (1, 2, 4, 8) if h % px == 0 and (h // px) >= 16]
+
+
+@pytest.mark.parametrize("h,B", [(32, 64), (64, 300), (256, 4096), (256, 1000), (256, 64),
+                                 (512, 777), (1024, 1024), (128, 2048)])
+def test_backward_every_plan(mlp, h, B):
+    for px in _px_options(h):
+        with _env(MLP_PX=px):
+            _check_grad(mlp, h, B, n=6000, seed=px)
+
+
+@pytest.mark.parametrize("coherent", [False, True])
+def test_train_every_plan_matches_oracle_and_each_other(mlp, coherent):
+    n, h, B, E, lr = 3000, 256, 512, 2, 0.01        # 6 steps per epoch, tail of 440
+    d = datagen.make_data(n, h, epochs=E, shuffle=True, seed=91)
+    ref = oracle.train(d.X, d.Y, d.W1, d.W2, B, lr, E, perm=d.perm)
+    runs = {}
+    for px in _px_options(h):
+        with _env(MLP_PX=px, MLP_FORCE_COHERENT=1 if coherent else None):
+            runs[px] = _train_gpu(mlp, d, B, lr, E, perm=d.perm)
+    for px, (g1, g2, gsl, gel) in runs.items():
+        assert rel(g1 - d.W1, ref["W1"] - d.W1.astype(np.float64)) <= 1e-3, px
+        assert rel(g2 - d.W2, ref["W2"] - d.W2.astype(np.float64)) <= 1e-3, px
+        assert np.all(np.abs(gsl - ref["step_loss"]) <= 1e-3 * ref["step_loss"]), px
+        assert np.all(np.abs(gel - ref["epoch_loss"]) <= 1e-3 * ref["epoch_loss"]), px
+
+
+def test_coherent_fallback_is_bitwise_identical(mlp):
+    n, h, B, E, lr = 2000, 256, 256, 2, 0.01
+    d = datagen.make_data(n, h, epochs=E, shuffle=True, seed=92)
+    for px in (1, 8):
+        with _env(MLP_PX=px):
+            a = _train_gpu(mlp, d, B, lr, E, perm=d.perm)
+        with _env(MLP_PX=px, MLP_FORCE_COHERENT=1):
+            b = _train_gpu(mlp, d, B, lr, E, perm=d.perm)
+        for x, y in zip(a, b):
+            assert np.array_equal(x, y)
+
+
+@pytest.mark.parametrize("h,B", [(256, 256), (1024, 1024), (32, 100)])
+def test_tile_path_matches_oracle(mlp, h, B):
+    with _env(MLP_PATH="tile"):
+        _check_grad(mlp, h, B, n=5000, seed=3)
+        n, E, lr = 1500, 2, 0.01
+        d = datagen.make_data(n, h, epochs=E, shuffle=True, seed=93 + h)
+        g1, g2, gsl, gel = _train_gpu(mlp, d, B, lr, E, perm=d.perm)
+    ref = oracle.train(d.X, d.Y, d.W1, d.W2, B, lr, E, perm=d.perm)
+    assert rel(g1 - d.W1, ref["W1"] - d.W1.astype(np.float64)) <= 1e-3
+    assert np.all(np.abs(gel - ref["epoch_loss"]) <= 1e-3 * ref["epoch_loss"])
+
+
+def test_launch_info_single_launch(mlp):
+    d = datagen.make_data(64, 256, seed=4, with_perm=False)
+    ctx, _, _ = _ctx(mlp, d.W1, d.W2, 4096)
+    wg, launches = mlp.mlp_launch_info(ctx, 10_000_000, 4096, 3)
+    assert launches == 1 and wg == 256
+    with _env(MLP_PATH="tile"):
+        wg, launches = mlp.mlp_launch_info(ctx, 10_000, 4096, 3)
+    assert launches == 2 * 3 * 3 + 1
+
+
+def test_workspace_reused_by_a_new_context(mlp):
+    """A workspace that held another context's exchange words must not leak them
+    into a new context (regression: stale step tags matched the new call's tags)."""
+    d = datagen.make_data(5000, 256, epochs=1, shuffle=True, seed=61)
+    need = mlp.mlp_workspace_bytes(32, 256, 4096)
+    ws = torch.empty(need, dtype=torch.uint8, device="cuda")
+    X, Y = _to(d.X), _to(d.Y)
+    for trial in range(3):
+        w1 = _to(d.W1)
+        w2 = _to(d.W2)
+        ctx = mlp.mlp_init(w1, w2, 4096, workspace=ws)
+        if trial == 0:
+            mlp.mlp_train_epochs(ctx, X, Y, 1000, 0.01, 1, perm=_to(d.perm))
+        idx = np.arange(4096, dtype=np.int32)
+        w1.copy_(_to(d.W1))
+        w2.copy_(_to(d.W2))
+        dW1, dW2, _ = mlp.mlp_backward(ctx, X, Y, _to(idx))
+        torch.cuda.synchronize()
+        mlp.mlp_check_errors(ctx)
+        r1, r2, _, z, zabs = oracle.grad(d.X, d.Y, d.W1, d.W2, idx=idx, want_z=True)
+        yp = oracle.forward(d.X, d.W1, d.W2, idx=idx)
+        g1 = dW1.cpu().numpy()
+        r1a, _, _ = align_kinks(g1, r1, d.X, d.Y, d.W1.astype(np.float64),
+                                d.W2.astype(np.float64), idx, z, zabs, yp)
+        assert rel(g1, r1a) <= 1e-4 and rel(dW2.cpu().numpy(), r2) <= 1e-4
+        del ctx
