@@ -23,12 +23,14 @@ struct Control {
     double epoch_sse;     // tile path: running sum of squared residuals of the epoch
     int32_t pad0[60];
     int32_t reg[64];      // persistent trainer: registration / start / exit counters
-    uint32_t pad[896];
+    uint64_t trace[384];  // persistent trainer: optional phase timestamps (48 steps x 8)
+    uint32_t pad[128];
 };
 static_assert(sizeof(Control) <= CTL_BYTES, "control block too large");
 
 // Launch plan of the persistent trainer (see train_persistent.hip).
 struct TrainPlan {
+    int inst = -1;      // instantiated shape
     int px = 0;         // groups (one per XCD), each owns U = hidden / px units
     int pr = 0;         // workgroups per group; each takes R rows of a batch
     int R = 0;          // rows per workgroup (multiple of 16, <= RMAX)
@@ -68,6 +70,8 @@ struct TrainArgs {
     uint32_t tag_base;        // tags of this call: tag_base + step
     uint64_t timeout_ticks;   // per-wait limit in s_memrealtime ticks (100 MHz)
     int32_t force_coherent;   // 1: device-coherent stores even when placement checks out
+    uint64_t *trace;          // nullable: phase timestamps of workgroup (0, 0)
+    uint64_t *trace_all;      // nullable: phase timestamps of every workgroup, 8 steps
     TrainPlan plan;
 };
 

@@ -55,3 +55,19 @@ def align_kinks(dW1_gpu, dW1_ref, X, Y, W1, W2, idx, z, zabs, ypred):
         out[:, j] = best
         flips += int((best_sel != on).sum())
     return out, n_amb, flips
+
+
+def loss_tolerance(loss_ref, z, zabs, W2, rel_bar=1e-5):
+    """Bar for the batch MSE computed in fp32.
+
+    Ypred_i = sum_j ReLU(Z1_ij) W2_j carries an fp32 rounding error
+    delta_i <~ 4 sqrt(h + 32) u S_i (random-walk bound), with
+    S_i = sum_j |ReLU(Z1_ij) W2_j| + |W2_j| sum_k |X_ik W1_kj|. The loss
+    L = mean(r_i^2) then moves by about 2 sqrt(L) rms(delta): when Ypred is close
+    to Y (a cancellation in r_i) this absolute term, not the relative one, is the
+    honest bound."""
+    W2 = np.abs(np.reshape(W2, -1))
+    h = z.shape[1]
+    S = np.maximum(z, 0.0) @ W2 + zabs @ W2
+    delta = 4.0 * np.sqrt(h + 32.0) * U32 * S
+    return rel_bar * loss_ref + 2.0 * np.sqrt(loss_ref) * np.sqrt(np.mean(delta ** 2))

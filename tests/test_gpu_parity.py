@@ -2,7 +2,8 @@
 
 Tolerances (normwise relative error unless stated):
   - per-step gradients dW1, dW2: <= 1e-4, after ReLU-kink alignment of dW1;
-  - batch loss and forward outputs: <= 1e-5;
+  - forward outputs: <= 1e-5; batch loss: 1e-5 relative plus the fp32 forward
+    rounding term of tests/parity.py:loss_tolerance (matters where Ypred ~ Y);
   - weights and per-step losses after 10 SGD steps: <= 1e-3. The weight change
     W10 - W0 is also held to 1e-3, which is the meaningful check since
     lr * dW is small against W. The 32-1024-1 workload at lr 0.005 is the
@@ -17,7 +18,7 @@ import torch
 
 import datagen
 import oracle
-from tests.parity import align_kinks, rel
+from tests.parity import align_kinks, loss_tolerance, rel
 
 pytestmark = pytest.mark.gpu
 
@@ -85,7 +86,7 @@ def _check_grad(mlp, h, B, n=5000, seed=0, idx_none=False):
     e1, e2 = rel(g1, r1a), rel(g2, r2)
     assert e1 <= 1e-4, (e1, n_amb, flips)
     assert e2 <= 1e-4, e2
-    assert abs(gl - rL) <= 1e-5 * rL
+    assert abs(gl - rL) <= loss_tolerance(rL, z, zabs, W2)
     return e1, e2
 
 
@@ -299,32 +300,50 @@ def _env(**kv):
                 os.environ[k] = v
 
 
-def _px_options(h):
-    return [px for px in (1, 2, 4, 8) if h % px == 0 and (h // px) >= 16]
+# The fused trainer's instantiated shapes: (groups PX, workgroups per group PR,
+# rows per workgroup R, units per group U); hidden = PX * U, batch <= PR * R.
+FUSED_SHAPES = [(8, 32, 128, 32), (8, 32, 64, 32), (8, 32, 32, 32), (4, 32, 16, 64),
+                (1, 16, 16, 256), (8, 32, 32, 128), (8, 32, 16, 128),
+                (8, 32, 16, 64), (2, 16, 16, 64), (1, 16, 16, 64), (1, 8, 32, 32),
+                (4, 16, 16, 64), (2, 16, 16, 128)]
+# Index = position in the library's shape table. A one-XCD shape with four
+# workgroups of 64 owned units each, (1, 4, 16, 256), is disabled: its
+# gradient sums came out wrong from the second SGD step on, and one run of it
+# faulted the GPU; the cause is not found yet, so it is not instantiated.
 
 
-@pytest.mark.parametrize("h,B", [(32, 64), (64, 300), (256, 4096), (256, 1000), (256, 64),
-                                 (512, 777), (1024, 1024), (128, 2048)])
-def test_backward_every_plan(mlp, h, B):
-    for px in _px_options(h):
-        with _env(MLP_PX=px):
-            _check_grad(mlp, h, B, n=6000, seed=px)
+@pytest.mark.skip(reason="shape (1, 4, 16, 256) disabled: wrong sums from step 2 and one GPU "
+                         "fault, cause not yet found; not instantiated in the library")
+def test_disabled_shape_four_workgroups_one_xcd():
+    pass
 
 
-@pytest.mark.parametrize("coherent", [False, True])
-def test_train_every_plan_matches_oracle_and_each_other(mlp, coherent):
-    n, h, B, E, lr = 3000, 256, 512, 2, 0.01        # 6 steps per epoch, tail of 440
-    d = datagen.make_data(n, h, epochs=E, shuffle=True, seed=91)
+@pytest.mark.parametrize("inst", range(len(FUSED_SHAPES)))
+def test_backward_every_fused_shape(mlp, inst):
+    px, pr, r, u = FUSED_SHAPES[inst]
+    h, cap = px * u, pr * r
+    with _env(MLP_INST=inst):
+        d = datagen.make_data(64, h, seed=4, with_perm=False)
+        ctx, _, _ = _ctx(mlp, d.W1, d.W2, cap)
+        wg, launches = mlp.mlp_launch_info(ctx, cap, cap, 1)
+        assert (wg, launches) == (8 * pr, 1), "shape table out of step with the library"
+        for B in sorted({cap, cap - 7, cap // 2 + 3, 1}):
+            _check_grad(mlp, h, B, n=max(6000, cap), seed=inst * 7 + B)
+
+
+@pytest.mark.parametrize("inst", range(len(FUSED_SHAPES)))
+def test_train_every_fused_shape(mlp, inst):
+    px, pr, r, u = FUSED_SHAPES[inst]
+    h, B = px * u, pr * r
+    n, E, lr = 3 * B - 5, 2, 0.005                 # a short tail batch every epoch
+    d = datagen.make_data(n, h, epochs=E, shuffle=True, seed=300 + inst)
+    with _env(MLP_INST=inst):
+        g1, g2, gsl, gel = _train_gpu(mlp, d, B, lr, E, perm=d.perm)
     ref = oracle.train(d.X, d.Y, d.W1, d.W2, B, lr, E, perm=d.perm)
-    runs = {}
-    for px in _px_options(h):
-        with _env(MLP_PX=px, MLP_FORCE_COHERENT=1 if coherent else None):
-            runs[px] = _train_gpu(mlp, d, B, lr, E, perm=d.perm)
-    for px, (g1, g2, gsl, gel) in runs.items():
-        assert rel(g1 - d.W1, ref["W1"] - d.W1.astype(np.float64)) <= 1e-3, px
-        assert rel(g2 - d.W2, ref["W2"] - d.W2.astype(np.float64)) <= 1e-3, px
-        assert np.all(np.abs(gsl - ref["step_loss"]) <= 1e-3 * ref["step_loss"]), px
-        assert np.all(np.abs(gel - ref["epoch_loss"]) <= 1e-3 * ref["epoch_loss"]), px
+    assert rel(g1 - d.W1, ref["W1"] - d.W1.astype(np.float64)) <= 1e-3
+    assert rel(g2 - d.W2, ref["W2"] - d.W2.astype(np.float64)) <= 1e-3
+    assert np.all(np.abs(gsl - ref["step_loss"]) <= 1e-3 * ref["step_loss"])
+    assert np.all(np.abs(gel - ref["epoch_loss"]) <= 1e-3 * ref["epoch_loss"])
 
 
 def test_coherent_fallback_is_bitwise_identical(mlp):
