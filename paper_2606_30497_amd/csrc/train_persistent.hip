@@ -70,16 +70,20 @@ struct Shape {
     static constexpr int NUW = NU / WU;                    // unit tiles per wave (stride WU)
     static constexpr int NRW = RTW * 16;                   // rows per wave
     static constexpr int UPW = U / PR;                     // units owned per workgroup
-    static constexpr int NPAIR = UPW * 32;                 // owned (k, unit) pairs
-    static constexpr int OWN_T = NPAIR >= 256 ? 256 : (NPAIR >= 64 ? NPAIR : 64);
-    static constexpr int SPLIT = NPAIR >= 64 ? 1 : 64 / NPAIR;   // partial-range splits
-    static constexpr int TPS = OWN_T / SPLIT;              // owner threads per split
-    static constexpr int PPT = NPAIR / TPS;                // pairs per owner thread
-    static constexpr int LPS = PR / SPLIT;                 // partials per split
-    static constexpr int ASPL0 = 64 / NRW;                 // exchange-A lane splits
-    static constexpr int ASPL = ASPL0 < PX ? ASPL0 : PX;
-    static constexpr int APPS = PX / ASPL;                 // peers per exchange-A lane
-    static_assert(ASPL == 1 || ASPL == 2 || ASPL == 4, "exchange-A lane splits");
+    static constexpr int NPAIR = UPW * 32;                 // owned (k, unit) words
+    static constexpr int KP = NPAIR / 2;                   // owned (k pair, unit) items
+    static constexpr int KPW = KP / 4 > 16 ? KP / 4 : 16;  // k pairs per owner wave
+    static constexpr int NWO = KP / KPW;                   // owner waves
+    static constexpr int OWN_T = 64 * NWO;                 // owner threads
+    static constexpr int SG = 64 / KPW;                    // source groups in an owner wave
+    static constexpr int LPS = PR / SG;                    // sources per owner lane
+    static constexpr int NPR = NRW / 2;                    // row pairs per wave
+    static constexpr int AG0 = 64 / NPR;                   // exchange-A lane groups
+    static constexpr int AG = AG0 < PX ? AG0 : PX;
+    static constexpr int APL = PX / AG;                    // peers per exchange-A lane
+    static_assert(KP % 16 == 0 && KPW * NWO == KP && NWO >= 1 && NWO <= NCW && KPW <= 64 &&
+                      PR % SG == 0 && (SG == 1 || SG == 2 || SG == 4), "ownership");
+    static_assert(AG == 1 || AG == 2 || AG == 4 || AG == 8, "exchange-A lane groups");
     static constexpr int XS = 36;                          // X tile row stride (floats)
     static constexpr int WS = 36;                          // weight slice row stride
     static constexpr int PS = U + 1;                       // P partial row stride
@@ -100,7 +104,7 @@ struct Shape {
     static_assert(WR * WU == NCW && NR % WR == 0 && NU % WU == 0, "wave split");
     static_assert(NUW >= 1 && RTW >= 1 && NUW * RTW <= 8, "mask bits");
     static_assert(NRW == 16 || NRW == 32 || NRW == 64, "exchange-A lanes");
-    static_assert(U % PR == 0 && UPW >= 1 && NPAIR % TPS == 0 && PR % SPLIT == 0, "ownership");
+    static_assert(U % PR == 0 && UPW >= 1, "units per workgroup");
     static_assert(RSW % 256 == 0, "exchange-B stores");
     static_assert(R <= RMAX && R <= 128, "rows");
     static_assert(PX == 1 || PX == 2 || PX == 4 || PX == 8, "groups");
@@ -126,19 +130,43 @@ __device__ __forceinline__ uint64_t pack(float v, uint32_t tag) {
 __device__ __forceinline__ uint32_t tag_of(uint64_t w) { return (uint32_t)(w >> 32); }
 __device__ __forceinline__ float val_of(uint64_t w) { return __uint_as_float((uint32_t)w); }
 
-// device-coherent store / load (sc1)
-__device__ __forceinline__ void st_dev(uint64_t *p, uint64_t v) {
-    __hip_atomic_store(p, v, __ATOMIC_RELAXED, __HIP_MEMORY_SCOPE_AGENT);
+// Exchange words live in three buffers addressed through buffer resources
+// (32-bit byte offsets). A load outside a buffer returns 0, which never carries a
+// current tag, so a wrong offset shows up as a timeout, not as a stray access.
+typedef __amdgpu_buffer_rsrc_t rsrc_t;
+typedef int i2v __attribute__((ext_vector_type(2)));
+typedef int i4v __attribute__((ext_vector_type(4)));
+constexpr int CPOL_SC1 = 16;   // cache policy: device-coherent (sc1)
+
+__device__ __forceinline__ rsrc_t make_rsrc(void *p, uint32_t bytes) {
+    return __builtin_amdgcn_make_buffer_rsrc(p, (short)0, (int)bytes, 0x00020000);
 }
-__device__ __forceinline__ uint64_t ld_dev(const uint64_t *p) {
-    return __hip_atomic_load(const_cast<uint64_t *>(p), __ATOMIC_RELAXED, __HIP_MEMORY_SCOPE_AGENT);
+struct W2 {   // two adjacent tagged words
+    uint64_t a, b;
+};
+__device__ __forceinline__ uint64_t join(int lo, int hi) {
+    return (uint64_t)(uint32_t)lo | ((uint64_t)(uint32_t)hi << 32);
 }
-// XCD-local store: plain (lands in the XCD's L2) or device-coherent
-__device__ __forceinline__ void st_loc(uint64_t *p, uint64_t v, bool plain) {
-    if (plain)
-        __hip_atomic_store(p, v, __ATOMIC_RELAXED, __HIP_MEMORY_SCOPE_SINGLETHREAD);
+// device-coherent loads of one / two adjacent words
+__device__ __forceinline__ uint64_t ld1(rsrc_t r, uint32_t off) {
+    const i2v v = __builtin_amdgcn_raw_buffer_load_b64(r, off, 0, CPOL_SC1);
+    return join(v.x, v.y);
+}
+__device__ __forceinline__ W2 ld2(rsrc_t r, uint32_t off) {
+    const i4v v = __builtin_amdgcn_raw_buffer_load_b128(r, off, 0, CPOL_SC1);
+    return W2{join(v.x, v.y), join(v.z, v.w)};
+}
+// store of one word: device-coherent (dev) or plain (lands in the XCD's L2)
+__device__ __forceinline__ void st1(rsrc_t r, uint32_t off, uint64_t w, bool dev) {
+    const i2v v = {(int)(uint32_t)w, (int)(uint32_t)(w >> 32)};
+    if (dev)
+        __builtin_amdgcn_raw_buffer_store_b64(v, r, off, 0, CPOL_SC1);
     else
-        st_dev(p, v);
+        __builtin_amdgcn_raw_buffer_store_b64(v, r, off, 0, 0);
+}
+__device__ __forceinline__ uint32_t stale(uint64_t w, uint32_t tag) { return tag_of(w) ^ tag; }
+__device__ __forceinline__ uint32_t stale(const W2 &w, uint32_t tag) {
+    return (tag_of(w.a) ^ tag) | (tag_of(w.b) ^ tag);
 }
 
 // Order LDS traffic between the lanes of one wave (no workgroup barrier).
@@ -181,17 +209,16 @@ struct Waiter {
         }
         if (aborted) *stamp = step + 1;
     }
-    // w[i] was loaded from p + i * STRIDE; reload the words until every tag is
-    // current. The retry path rebuilds its addresses from p, so no per-word
-    // address stays live in registers.
-    template <int N, int STRIDE>
-    __device__ __forceinline__ void settle(uint64_t (&w)[N], const uint64_t *p, uint32_t tag) {
+    // w[i] holds a loaded word (or word pair); reload(i) loads it again. Wait
+    // until every tag is current.
+    template <int N, class T, class Reload>
+    __device__ __forceinline__ void settle(T (&w)[N], uint32_t tag, Reload reload) {
         uint32_t spins = 0;
         uint64_t deadline = 0;
         while (true) {
             uint32_t bad = 0;
 #pragma unroll
-            for (int i = 0; i < N; ++i) bad |= tag_of(w[i]) ^ tag;
+            for (int i = 0; i < N; ++i) bad |= stale(w[i], tag);
             if (bad == 0 || aborted) break;
             if (spins == 0) deadline = now_ticks() + COLD(timeout_ticks);
             if ((++spins & 63u) == 0) {
@@ -199,31 +226,30 @@ struct Waiter {
                 if (aborted) break;
             }
             __builtin_amdgcn_s_sleep(1);
-            const uint64_t *q = p;
-            asm volatile("" : "+v"(q));
-            if constexpr (N == 1) {
-                w[0] = ld_dev(q);
-            } else {
+            asm volatile("" ::: "memory");   // the reloads are not the loads above
 #pragma unroll
-                for (int i = 0; i < N; ++i) w[i] = ld_dev(q + i * STRIDE);
-            }
+            for (int i = 0; i < N; ++i) w[i] = reload(i);
         }
     }
 };
 
-// C words per thread of the all-gathered weight slice ([unit][33] words, word
-// i at src + 256 q for i = i0 + 256 q) into the LDS slice ([unit][WS] floats).
+// C word pairs per thread of the all-gathered weight slice ([unit][33] words;
+// pair i = i0 + 256 q at byte offset base + 16 i) into the LDS slice ([unit][WS]).
 template <int C, int WS>
-__device__ __forceinline__ void gather_slice(Waiter &wt, const uint64_t *src, float *Wsl, int i0,
+__device__ __forceinline__ void gather_slice(Waiter &wt, rsrc_t r, uint32_t base, float *Wsl, int i0,
                                              uint32_t tag) {
-    uint64_t w[C];
+    W2 w[C];
+    auto reload = [&](int q) { return ld2(r, base + 16u * (uint32_t)(i0 + 256 * q)); };
 #pragma unroll
-    for (int q = 0; q < C; ++q) w[q] = ld_dev(src + 256 * q);
-    wt.settle<C, 256>(w, src, tag);
+    for (int q = 0; q < C; ++q) w[q] = reload(q);
+    wt.settle(w, tag, reload);
 #pragma unroll
     for (int q = 0; q < C; ++q) {
-        const int i = i0 + 256 * q, jl = i / 33, k = i - jl * 33;
-        Wsl[jl * WS + k] = val_of(w[q]);
+        const int i = 2 * (i0 + 256 * q);
+        const int j0 = i / 33, k0 = i - j0 * 33;
+        const int j1 = (i + 1) / 33, k1 = i + 1 - j1 * 33;
+        Wsl[j0 * WS + k0] = val_of(w[q].a);
+        Wsl[j1 * WS + k1] = val_of(w[q].b);
     }
 }
 
@@ -240,6 +266,13 @@ __device__ __forceinline__ float row16_sum(float v) {
 // Butterfly sums (every lane gets the total, in a fixed order).
 __device__ __forceinline__ float sum32(float v) {
     v += __shfl_xor(v, 16, 64);
+    v += __shfl_xor(v, 8, 64);
+    v += __shfl_xor(v, 4, 64);
+    v += __shfl_xor(v, 2, 64);
+    v += __shfl_xor(v, 1, 64);
+    return v;
+}
+__device__ __forceinline__ float sum16(float v) {
     v += __shfl_xor(v, 8, 64);
     v += __shfl_xor(v, 4, 64);
     v += __shfl_xor(v, 2, 64);
@@ -266,17 +299,18 @@ struct Pos {
 // first TRACE_STEPS steps, or every workgroup for steps [16, 24).
 constexpr int TRACE_STEPS = 48;
 constexpr int TRACE_ALL_FIRST = 16, TRACE_ALL_STEPS = 8;
-#define TRACE(ph)                                                                          \
+#define TRACE_BY(ph, t0)                                                                   \
     do {                                                                                   \
         if constexpr (TR)                                                                  \
-        if (a.trace && tid == 0 && gx == 0 && gb == 0 && s < TRACE_STEPS)                  \
+        if (a.trace && tid == (t0) && gx == 0 && gb == 0 && s < TRACE_STEPS)               \
             a.trace[s * 8 + (ph)] = now_ticks();                                           \
         if constexpr (TR)                                                                  \
-        if (a.trace_all && tid == 0 && s >= TRACE_ALL_FIRST &&                             \
+        if (a.trace_all && tid == (t0) && s >= TRACE_ALL_FIRST &&                          \
             s < TRACE_ALL_FIRST + TRACE_ALL_STEPS)                                         \
             a.trace_all[((gx * S::PR + gb) * TRACE_ALL_STEPS + (s - TRACE_ALL_FIRST)) * 8 + \
                         (ph)] = now_ticks();                                               \
     } while (0)
+#define TRACE(ph) TRACE_BY(ph, 0)
 
 // ---------------------------------------------------------------------------
 // The kernel
@@ -288,7 +322,8 @@ constexpr int TRACE_ALL_FIRST = 16, TRACE_ALL_STEPS = 8;
 template <class S, bool TR>
 __global__ __launch_bounds__(NTHR) void k_train(const TrainArgs a) {
     extern __shared__ __attribute__((aligned(16))) float lds[];
-    __shared__ int s_flags[8];   // 0: group x, 1: rank b, 2: plain local stores, 3: abort stamp, 4: active
+    __shared__ int s_flags[8];   // 0: group x, 1: rank b, 2: plain local stores, 3: abort stamp, 4: active,
+                                 // 5: forward-done stamp (step + 1) of wave 0
 
     constexpr int R = S::R, U = S::U, PR = S::PR, PX = S::PX, H = S::H;
     constexpr int WR = S::WR, WU = S::WU, NUW = S::NUW, RTW = S::RTW, NRW = S::NRW;
@@ -346,7 +381,10 @@ __global__ __launch_bounds__(NTHR) void k_train(const TrainArgs a) {
     const bool run = __builtin_amdgcn_readfirstlane(s_flags[4]) != 0 &&
                      __builtin_amdgcn_readfirstlane(s_flags[3]) == 0;
     __syncthreads();
-    if (tid == 0) s_flags[3] = 0;   // from here on: the abort stamp
+    if (tid == 0) {
+        s_flags[3] = 0;   // from here on: the abort stamp
+        s_flags[5] = 0;
+    }
 
     float *Xall = lds + S::O_X;     // [2][R][XS]
     float *Yall = lds + S::O_Y;     // [2][R]
@@ -372,18 +410,25 @@ __global__ __launch_bounds__(NTHR) void k_train(const TrainArgs a) {
 
         if (wave < NCW) {
             // ================= compute waves =================================
+            // exchange buffers: A [2][PR][PX][RMAX], B [2][PX][GBW], C [2][PX][U*33] words
+            const rsrc_t rA = make_rsrc(a.xch, 8u * (uint32_t)(2 * PR * PX * RMAX));
+            const rsrc_t rB = make_rsrc(a.rs, 8u * (uint32_t)(2 * PX * S::GBW));
+            const rsrc_t rC = make_rsrc(a.ag, 8u * (uint32_t)(2 * PX * U * 33));
             const int wr = wave % WR, wu = wave / WR;
-            const bool owner = tid < S::OWN_T;
-            const int osplit = tid / S::TPS, ot = tid % S::TPS;
-            float ow1[S::PPT], ow2[S::PPT];   // master copy of the owned pairs
+            constexpr int KPW = S::KPW, SG = S::SG, LPS = S::LPS;
+            // the owner waves are the last NWO compute waves (the loader shares SIMD 0
+            // with wave 0)
+            constexpr int OW0 = NCW - S::NWO;
+            const bool owner = wave >= OW0;
+            const int kp = (wave - OW0) * KPW + lane % KPW;     // owned k pair
+            const int sg = lane / KPW;                          // source group
+            const int jl = kp >> 4, k0 = 2 * (kp & 15);         // owned unit, first k of the pair
+            const int ug = gx * U + gb * UPW + jl;
+            float ow1a = 0.f, ow1b = 0.f, ow2 = 0.f;            // master copy of the owned words
             if (owner) {
-#pragma unroll
-                for (int q = 0; q < S::PPT; ++q) {
-                    const int p = ot + S::TPS * q, jl = p >> 5, k = p & 31;
-                    const int ug = gx * U + gb * UPW + jl;
-                    ow1[q] = COLD(W1)[k * H + ug];
-                    ow2[q] = COLD(W2)[ug];
-                }
+                ow1a = COLD(W1)[k0 * H + ug];
+                ow1b = COLD(W1)[(k0 + 1) * H + ug];
+                ow2 = COLD(W2)[ug];
             }
             // the loss is reduced one step late by wave 1 of workgroup (0, 0)
             const bool lossw = gx == 0 && gb == 0 && wave == 1;
@@ -391,9 +436,10 @@ __global__ __launch_bounds__(NTHR) void k_train(const TrainArgs a) {
             Pos cur{0, 0}, prev{0, 0};
             int nb_prev = 1;
             int done = 0;
-            const int rl = lane % NRW;             // row within the wave's rows
-            const int rw = wr * NRW + rl;          // row within the workgroup
-            __syncthreads();                       // weights and the first rows staged
+            const int pr2 = lane % S::NPR;                      // row pair within the wave
+            const int ra = wr * NRW + 2 * pr2;                  // first row of the pair (workgroup)
+            const int agi = (lane / S::NPR) % S::AG;            // exchange-A peer group
+            __syncthreads();                                    // weights and the first rows staged
 
             for (int s = 0; s < steps; ++s) {
                 {
@@ -408,15 +454,15 @@ __global__ __launch_bounds__(NTHR) void k_train(const TrainArgs a) {
                 const float scale = 2.0f / (float)nb;
                 const float *Xb = Xall + par * R * XS;
                 const float *Yb = Yall + par * R;
-                uint64_t *rsg = a.rs + (size_t)(par * PX + gx) * S::GBW;
+                const uint32_t bB = 8u * (uint32_t)((par * PX + gx) * S::GBW);   // group block (bytes)
                 TRACE(0);
 
                 // deferred loss: issue the loads of the previous step's SSE partials
                 const uint32_t tag_prev = tag - 1;
-                const uint64_t *sse_prev = a.rs + (size_t)((par ^ 1) * PX) * S::GBW + PR * S::RSW +
-                                           (lane < PR ? lane : 0);
+                const uint32_t sse_prev = 8u * (uint32_t)(((par ^ 1) * PX) * S::GBW + PR * S::RSW +
+                                                          (lane < PR ? lane : 0));
                 uint64_t sw[1] = {pack(0.f, tag_prev)};
-                if (lossw && s > 0 && lane < PR) sw[0] = ld_dev(sse_prev);
+                if (lossw && s > 0 && lane < PR) sw[0] = ld1(rB, sse_prev);
 
                 // ---- 1. forward: Z1 tiles, mask bits, partial Ypred ---------------
                 float w1b[NUW][8], w2v[NUW];
@@ -461,43 +507,58 @@ __global__ __launch_bounds__(NTHR) void k_train(const TrainArgs a) {
                         if (li == 15) Ypart[wu * R + tile * 16 + 4 * lq + v] = sv;
                     }
                 }
+                if (wave == 0 && lane == 0) s_flags[5] = s + 1;   // the loader may start
                 if constexpr (WU > 1)
                     __syncthreads();   // partial Ypred of the unit waves
                 else
                     wave_sync();
-                float yv = 0.f;
-#pragma unroll
-                for (int w = 0; w < WU; ++w) yv += Ypart[w * R + rw];
                 TRACE(1);
 
                 // ---- 2. exchange A: partial Ypred across groups ------------------
+                // lane: rows (ra, ra + 1), peers agi * APL + x; sums in group order
+                float y0 = 0.f, y1 = 0.f;
                 if constexpr (PX > 1) {
-                    uint64_t *xa = a.xch + (size_t)((par * PR + gb) * PX) * RMAX;
-                    if (wu == 0 && lane < NRW) st_dev(xa + gx * RMAX + rw, pack(yv, tag));
-                    const int sp = (lane / NRW) % S::ASPL;
-                    const uint64_t *src = xa + (size_t)(sp * S::APPS) * RMAX + rw;
-                    uint64_t w[S::APPS];
+                    const uint32_t bA = 8u * (uint32_t)((par * PR + gb) * PX * RMAX);
+                    if (wu == 0 && lane < NRW) {
+                        float v = 0.f;
 #pragma unroll
-                    for (int x = 0; x < S::APPS; ++x) w[x] = ld_dev(src + x * RMAX);
-                    wt.settle<S::APPS, RMAX>(w, src, tag);
-                    float t = 0.f;
+                        for (int w = 0; w < WU; ++w) v += Ypart[w * R + wr * NRW + lane];
+                        st1(rA, bA + 8u * (uint32_t)(gx * RMAX + wr * NRW + lane), pack(v, tag), true);
+                    }
+                    asm volatile("" ::: "memory");
+                    W2 w[S::APL];
+                    const uint32_t src = bA + 8u * (uint32_t)(agi * S::APL * RMAX + ra);
+                    auto reload = [&](int x) { return ld2(rA, src + 8u * (uint32_t)(x * RMAX)); };
 #pragma unroll
-                    for (int x = 0; x < S::APPS; ++x) t += val_of(w[x]);
-                    if constexpr (S::ASPL >= 2) t += __shfl_xor(t, NRW, 64);
-                    if constexpr (S::ASPL >= 4) t += __shfl_xor(t, 2 * NRW, 64);
-                    yv = t;
+                    for (int x = 0; x < S::APL; ++x) w[x] = reload(x);
+                    wt.settle(w, tag, reload);
+#pragma unroll
+                    for (int x = 0; x < S::APL; ++x) {
+                        y0 += val_of(w[x].a);
+                        y1 += val_of(w[x].b);
+                    }
+                    if constexpr (S::AG >= 2) { y0 += __shfl_xor(y0, S::NPR, 64); y1 += __shfl_xor(y1, S::NPR, 64); }
+                    if constexpr (S::AG >= 4) { y0 += __shfl_xor(y0, 2 * S::NPR, 64); y1 += __shfl_xor(y1, 2 * S::NPR, 64); }
+                    if constexpr (S::AG >= 8) { y0 += __shfl_xor(y0, 4 * S::NPR, 64); y1 += __shfl_xor(y1, 4 * S::NPR, 64); }
+                } else {
+#pragma unroll
+                    for (int w = 0; w < WU; ++w) {
+                        y0 += Ypart[w * R + ra];
+                        y1 += Ypart[w * R + ra + 1];
+                    }
                 }
                 TRACE(2);
 
                 // residual, dZ2 (eqs. 14-15), SSE of the wave's rows
                 {
-                    const float res = yv - Yb[rw];
-                    const bool in = rw < rc;
-                    const float g = in ? scale * res : 0.0f;
-                    const float r2 = (in && lane < NRW && wu == 0) ? res * res : 0.0f;
+                    const float e0 = y0 - Yb[ra], e1 = y1 - Yb[ra + 1];
+                    const bool in0 = ra < rc, in1 = ra + 1 < rc;
+                    const float g0 = in0 ? scale * e0 : 0.0f, g1 = in1 ? scale * e1 : 0.0f;
+                    const bool mine = lane < S::NPR && wu == 0;
+                    const float r2 = mine ? (in0 ? e0 * e0 : 0.0f) + (in1 ? e1 * e1 : 0.0f) : 0.0f;
                     const float sse = sum64(r2);
                     if (lane == 0) SseW[wave] = sse;
-                    if (lane < NRW) Gw[wave * NRW + rl] = g;
+                    if (lane < S::NPR) *reinterpret_cast<float2 *>(Gw + wave * NRW + 2 * pr2) = make_float2(g0, g1);
                     wave_sync();
                 }
 
@@ -537,7 +598,7 @@ __global__ __launch_bounds__(NTHR) void k_train(const TrainArgs a) {
 
                 // deferred loss of the previous step (its words are long written)
                 if (lossw && s > 0) {
-                    wt.settle<1, 0>(sw, sse_prev, tag_prev);
+                    wt.settle(sw, tag_prev, [&](int) { return lane < PR ? ld1(rB, sse_prev) : pack(0.f, tag_prev); });
                     const float sse = sum64(lane < PR ? val_of(sw[0]) : 0.0f);
                     if (lane == 0) {
                         const float L = sse / (float)nb_prev;               // eq. 14
@@ -553,8 +614,8 @@ __global__ __launch_bounds__(NTHR) void k_train(const TrainArgs a) {
                 TRACE(3);
 
                 // ---- 4. exchange B: reduce-scatter of P inside the group ---------
-                // word (ul, k) of this workgroup goes to owner o = ul / UPW at
-                // rsg + (o * PR + gb) * NPAIR + (ul % UPW) * 32 + k
+                // word (ul, k) of this workgroup goes to owner o = ul / UPW at word
+                // (o * PR + gb) * NPAIR + (ul % UPW) * 32 + k of the group block
 #pragma unroll
                 for (int i0 = 0; i0 < S::RSW; i0 += 256) {
                     const int i = i0 + tid;
@@ -562,78 +623,92 @@ __global__ __launch_bounds__(NTHR) void k_train(const TrainArgs a) {
                     float v = 0.f;
 #pragma unroll
                     for (int w = 0; w < WR; ++w) v += Pred[(w * 32 + k) * PS + ul];
-                    const int o = ul / UPW, jl = ul - o * UPW;
-                    st_loc(rsg + (size_t)(o * PR + gb) * NPAIR + jl * 32 + k, pack(v, tag), plain);
+                    const int o = ul / UPW, jo = ul - o * UPW;
+                    st1(rB, bB + 8u * (uint32_t)((o * PR + gb) * NPAIR + jo * 32 + k), pack(v, tag), !plain);
                 }
                 if (tid == 0) {
                     float v = 0.f;
 #pragma unroll
                     for (int w = 0; w < WR; ++w) v += SseW[w];
-                    st_loc(rsg + PR * S::RSW + gb, pack(gx == 0 ? v : 0.f, tag), plain);
+                    st1(rB, bB + 8u * (uint32_t)(PR * S::RSW + gb), pack(gx == 0 ? v : 0.f, tag), !plain);
                 }
+                asm volatile("" ::: "memory");
                 if (owner) {
-                    const uint64_t *ob = rsg + (size_t)(gb * PR + osplit * S::LPS) * NPAIR;
-                    uint64_t w[S::PPT][S::LPS];
+                    // words (k0, k0 + 1) of unit jl from sources sg * LPS + b, in source order
+                    // (in chunks of at most 8 sources, to bound registers)
+                    constexpr int CHB = LPS < 8 ? LPS : 8;
+                    static_assert(LPS % CHB == 0, "owner chunks");
+                    float p0 = 0.f, p1 = 0.f;
 #pragma unroll
-                    for (int q = 0; q < S::PPT; ++q)
+                    for (int c = 0; c < LPS / CHB; ++c) {
+                        const uint32_t ob =
+                            bB + 8u * (uint32_t)((gb * PR + sg * LPS + c * CHB) * NPAIR + 2 * kp);
+                        W2 w[CHB];
+                        auto reload = [&](int b) { return ld2(rB, ob + 8u * (uint32_t)(b * NPAIR)); };
 #pragma unroll
-                        for (int b = 0; b < S::LPS; ++b)
-                            w[q][b] = ld_dev(ob + b * NPAIR + ot + S::TPS * q);
-                    float pk[S::PPT];
+                        for (int b = 0; b < CHB; ++b) w[b] = reload(b);
+                        wt.settle(w, tag, reload);
 #pragma unroll
-                    for (int q = 0; q < S::PPT; ++q) {
-                        wt.settle<S::LPS, NPAIR>(w[q], ob + ot + S::TPS * q, tag);
-                        float t = 0.f;
-#pragma unroll
-                        for (int b = 0; b < S::LPS; ++b) t += val_of(w[q][b]);
-                        if constexpr (S::SPLIT == 2) t += __shfl_xor(t, 32, 64);
-                        pk[q] = t;
-                    }
-                    TRACE(4);
-                    // ---- update the owned units (eq. 19) or emit gradients ------
-                    uint64_t *agg = a.ag + (size_t)(par * PX + gx) * (U * 33);
-#pragma unroll
-                    for (int q = 0; q < S::PPT; ++q) {
-                        const int p = ot + S::TPS * q, jl = p >> 5, k = p & 31;
-                        const int ug = gx * U + gb * UPW + jl;
-                        const float w1 = ow1[q], w2 = ow2[q];
-                        const float dw1 = w2 * pk[q];                      // dW1_kj = W2_j P_kj
-                        const float dw2 = sum32(w1 * pk[q]);               // dW2_j = sum_k W1_kj P_kj
-                        if (a.mode == 1) {
-                            if (osplit == 0) {
-                                COLD(dW1)[k * H + ug] = dw1;
-                                if (k == 0) COLD(dW2)[ug] = dw2;
-                            }
-                        } else {
-                            ow1[q] = w1 - a.lr * dw1;
-                            ow2[q] = w2 - a.lr * dw2;
-                            if (osplit == 0) {
-                                st_loc(agg + (gb * UPW + jl) * 33 + k, pack(ow1[q], tag), plain);
-                                if (k == 0) st_loc(agg + (gb * UPW + jl) * 33 + 32, pack(ow2[q], tag), plain);
-                            }
+                        for (int b = 0; b < CHB; ++b) {
+                            p0 += val_of(w[b].a);
+                            p1 += val_of(w[b].b);
                         }
                     }
-                    TRACE(5);
+                    if constexpr (SG >= 2) { p0 += __shfl_xor(p0, KPW, 64); p1 += __shfl_xor(p1, KPW, 64); }
+                    if constexpr (SG >= 4) { p0 += __shfl_xor(p0, 2 * KPW, 64); p1 += __shfl_xor(p1, 2 * KPW, 64); }
+                    TRACE_BY(4, OW0 * 64);
+                    // ---- update the owned units (eq. 19) or emit gradients ------
+                    const float dw1a = ow2 * p0, dw1b = ow2 * p1;       // dW1_kj = W2_j P_kj
+                    const float dw2 = sum16(fmaf(ow1b, p1, ow1a * p0)); // dW2_j = sum_k W1_kj P_kj
+                    if (a.mode == 1) {
+                        if (sg == 0) {
+                            float *dW1 = COLD(dW1);
+                            dW1[k0 * H + ug] = dw1a;
+                            dW1[(k0 + 1) * H + ug] = dw1b;
+                            if (k0 == 0) COLD(dW2)[ug] = dw2;
+                        }
+                    } else {
+                        ow1a -= a.lr * dw1a;
+                        ow1b -= a.lr * dw1b;
+                        ow2 -= a.lr * dw2;
+                        if (sg == 0) {
+                            const uint32_t cb = 8u * (uint32_t)((par * PX + gx) * U * 33 + (gb * UPW + jl) * 33 + k0);
+                            st1(rC, cb, pack(ow1a, tag), !plain);
+                            st1(rC, cb + 8u, pack(ow1b, tag), !plain);
+                            if (k0 == 0) st1(rC, cb + 8u * 32u, pack(ow2, tag), !plain);
+                        }
+                    }
+                    TRACE_BY(5, OW0 * 64);
                 }
+                asm volatile("" ::: "memory");
 
                 // ---- 5. exchange C: all-gather the group's updated slice ---------
                 if (a.mode == 0) {
-                    // at most CH words per thread in flight, to bound registers
-                    const uint64_t *agg = a.ag + (size_t)(par * PX + gx) * (U * 33);
-                    constexpr int NW = U * 33, FULL = NW / 256, REST = NW % 256;
-                    constexpr int CH = FULL < 17 ? FULL : 16;
+                    // at most CH word pairs per thread in flight, to bound registers
+                    const uint32_t cbase = 8u * (uint32_t)((par * PX + gx) * U * 33);
+                    constexpr int NP = U * 33 / 2, FULL = NP / 256, REST = NP % 256;
+                    constexpr int CH = FULL < 9 ? FULL : 8;
                     constexpr int NCH = (FULL + CH - 1) / CH;
-                    uint64_t wt1[1] = {pack(0.f, tag)};
-                    if (REST > 0 && tid < REST) wt1[0] = ld_dev(agg + 256 * FULL + tid);
+                    static_assert((U * 33) % 2 == 0 && FULL >= 1, "slice pairs");
+                    W2 wr1[1] = {W2{pack(0.f, tag), pack(0.f, tag)}};
+                    auto reload1 = [&](int) {
+                        return tid < REST ? ld2(rC, cbase + 16u * (uint32_t)(256 * FULL + tid))
+                                          : W2{pack(0.f, tag), pack(0.f, tag)};
+                    };
+                    if (REST > 0) wr1[0] = reload1(0);
 #pragma unroll
                     for (int c = 0; c < NCH - 1; ++c)
-                        gather_slice<CH, WS>(wt, agg + tid + 256 * CH * c, Wsl, tid + 256 * CH * c, tag);
-                    gather_slice<FULL - (NCH - 1) * CH, WS>(wt, agg + tid + 256 * CH * (NCH - 1), Wsl,
-                                                            tid + 256 * CH * (NCH - 1), tag);
-                    if (REST > 0 && tid < REST) {
-                        wt.settle<1, 0>(wt1, agg + 256 * FULL + tid, tag);
-                        const int i = 256 * FULL + tid, jl = i / 33, k = i - jl * 33;
-                        Wsl[jl * WS + k] = val_of(wt1[0]);
+                        gather_slice<CH, WS>(wt, rC, cbase, Wsl, tid + 256 * CH * c, tag);
+                    gather_slice<FULL - (NCH - 1) * CH, WS>(wt, rC, cbase, Wsl, tid + 256 * CH * (NCH - 1), tag);
+                    if (REST > 0) {
+                        wt.settle(wr1, tag, reload1);
+                        if (tid < REST) {
+                            const int i = 2 * (256 * FULL + tid);
+                            const int j0 = i / 33, q0 = i - j0 * 33;
+                            const int j1 = (i + 1) / 33, q1 = i + 1 - j1 * 33;
+                            Wsl[j0 * WS + q0] = val_of(wr1[0].a);
+                            Wsl[j1 * WS + q1] = val_of(wr1[0].b);
+                        }
                     }
                 }
                 TRACE(6);
@@ -649,11 +724,11 @@ __global__ __launch_bounds__(NTHR) void k_train(const TrainArgs a) {
             if (!aborted && done > 0 && lossw) {
                 // loss of the last step
                 const uint32_t tag_last = a.tag_base + (uint32_t)(done - 1);
-                const uint64_t *sse_last = a.rs + (size_t)(((done - 1) & 1) * PX) * S::GBW +
-                                           PR * S::RSW + (lane < PR ? lane : 0);
-                uint64_t swl[1] = {pack(0.f, tag_last)};
-                if (lane < PR) swl[0] = ld_dev(sse_last);
-                wt.settle<1, 0>(swl, sse_last, tag_last);
+                const uint32_t sse_last = 8u * (uint32_t)((((done - 1) & 1) * PX) * S::GBW + PR * S::RSW +
+                                                          (lane < PR ? lane : 0));
+                auto reload = [&](int) { return lane < PR ? ld1(rB, sse_last) : pack(0.f, tag_last); };
+                uint64_t swl[1] = {reload(0)};
+                wt.settle(swl, tag_last, reload);
                 const float sse = sum64(lane < PR ? val_of(swl[0]) : 0.0f);
                 if (lane == 0) {
                     const float L = sse / (float)nb_prev;
@@ -668,14 +743,11 @@ __global__ __launch_bounds__(NTHR) void k_train(const TrainArgs a) {
                     }
                 }
             }
-            if (a.mode == 0 && owner && osplit == 0) {
-#pragma unroll
-                for (int q = 0; q < S::PPT; ++q) {
-                    const int p = ot + S::TPS * q, jl = p >> 5, k = p & 31;
-                    const int ug = gx * U + gb * UPW + jl;
-                    COLD(W1)[k * H + ug] = ow1[q];
-                    if (k == 0) COLD(W2)[ug] = ow2[q];
-                }
+            if (a.mode == 0 && owner && sg == 0) {
+                float *W1 = COLD(W1);
+                W1[k0 * H + ug] = ow1a;
+                W1[(k0 + 1) * H + ug] = ow1b;
+                if (k0 == 0) COLD(W2)[ug] = ow2;
             }
         } else {
             // ================= loader wave ====================================
@@ -758,6 +830,12 @@ __global__ __launch_bounds__(NTHR) void k_train(const TrainArgs a) {
                     if (st != 0 && st <= s) break;
                 }
                 if constexpr (WU > 1) __syncthreads();
+                // wait until wave 0 has finished its forward pass: the compute waves
+                // then wait on exchange A, and the loader's work stays off their path
+                {
+                    const volatile int *fd = &s_flags[5];
+                    while (*fd < s + 1) __builtin_amdgcn_s_sleep(1);
+                }
                 // registers hold the rows of step s+1 and the indices of step s+2
                 // (position q2)
                 if (s + 1 < steps) stage((s + 1) & 1);
