@@ -71,6 +71,19 @@ def cpu_baseline(w, data, max_seconds=15.0):
                       % (steps, samples)}
 
 
+def copy_calibration(mib):
+    """A plain copy of known size: each launch reads and writes mib MiB."""
+    import torch
+    n = mib * (1 << 20) // 4
+    src = torch.ones(n, dtype=torch.float32, device="cuda:0")
+    dst = torch.empty_like(src)
+    torch.cuda.synchronize()
+    for _ in range(4):
+        dst.copy_(src)
+    torch.cuda.synchronize()
+    print(json.dumps({"copy_calibration_bytes_per_launch": n * 4, "launches": 4}), flush=True)
+
+
 def main():
     ap = argparse.ArgumentParser()
     ap.add_argument("--gpus", type=int, default=1)
@@ -79,7 +92,13 @@ def main():
     ap.add_argument("--workload", type=int, default=4,
                     help="index into datagen.WORKLOADS (default: the 10M-sample 32-256-1 run)")
     ap.add_argument("--no-cpu-baseline", action="store_true")
+    ap.add_argument("--copy-calibration", type=int, default=0, metavar="MIB",
+                    help="run only a plain device copy of MIB MiB (4 launches), the reference "
+                         "for scaling the FETCH_SIZE / WRITE_SIZE counters")
     args = ap.parse_args()
+    if args.copy_calibration:
+        copy_calibration(args.copy_calibration)
+        return
     if args.gpus != 1:
         print("bench.py runs on one GPU only: this path is single-GPU by design "
               "(--gpus %d requested)" % args.gpus, file=sys.stderr)
