@@ -77,13 +77,8 @@ struct Shape {
     static constexpr int OWN_T = 64 * NWO;                 // owner threads
     static constexpr int SG = 64 / KPW;                    // source groups in an owner wave
     static constexpr int LPS = PR / SG;                    // sources per owner lane
-    static constexpr int NPR = NRW / 2;                    // row pairs per wave
-    static constexpr int AG0 = 64 / NPR;                   // exchange-A lane groups
-    static constexpr int AG = AG0 < PX ? AG0 : PX;
-    static constexpr int APL = PX / AG;                    // peers per exchange-A lane
     static_assert(KP % 16 == 0 && KPW * NWO == KP && NWO >= 1 && NWO <= NCW && KPW <= 64 &&
                       PR % SG == 0 && (SG == 1 || SG == 2 || SG == 4), "ownership");
-    static_assert(AG == 1 || AG == 2 || AG == 4 || AG == 8, "exchange-A lane groups");
     static constexpr int XS = 36;                          // X tile row stride (floats)
     static constexpr int WS = 36;                          // weight slice row stride
     static constexpr int PS = U + 1;                       // P partial row stride
@@ -436,9 +431,6 @@ __global__ __launch_bounds__(NTHR) void k_train(const TrainArgs a) {
             Pos cur{0, 0}, prev{0, 0};
             int nb_prev = 1;
             int done = 0;
-            const int pr2 = lane % S::NPR;                      // row pair within the wave
-            const int ra = wr * NRW + 2 * pr2;                  // first row of the pair (workgroup)
-            const int agi = (lane / S::NPR) % S::AG;            // exchange-A peer group
             __syncthreads();                                    // weights and the first rows staged
 
             for (int s = 0; s < steps; ++s) {
@@ -465,6 +457,10 @@ __global__ __launch_bounds__(NTHR) void k_train(const TrainArgs a) {
                 if (lossw && s > 0 && lane < PR) sw[0] = ld1(rB, sse_prev);
 
                 // ---- 1. forward: Z1 tiles, mask bits, partial Ypred ---------------
+                // With one unit wave per row block (WU == 1) the row sums go straight
+                // to exchange A, tile by tile; otherwise they meet in LDS first.
+                constexpr bool DIRECT = WU == 1 && PX > 1;
+                const uint32_t bA = 8u * (uint32_t)((par * PR + gb) * PX * RMAX);
                 float w1b[NUW][8], w2v[NUW];
 #pragma unroll
                 for (int u = 0; u < NUW; ++u) {
@@ -504,7 +500,13 @@ __global__ __launch_bounds__(NTHR) void k_train(const TrainArgs a) {
 #pragma unroll
                     for (int v = 0; v < 4; ++v) {
                         const float sv = row16_sum(yp[v]);
-                        if (li == 15) Ypart[wu * R + tile * 16 + 4 * lq + v] = sv;
+                        if (li == 15) {
+                            const int row = tile * 16 + 4 * lq + v;
+                            if constexpr (DIRECT)
+                                st1(rA, bA + 8u * (uint32_t)(gx * RMAX + row), pack(sv, tag), true);
+                            else
+                                Ypart[wu * R + row] = sv;
+                        }
                     }
                 }
                 if (wave == 0 && lane == 0) s_flags[5] = s + 1;   // the loader may start
@@ -512,65 +514,68 @@ __global__ __launch_bounds__(NTHR) void k_train(const TrainArgs a) {
                     __syncthreads();   // partial Ypred of the unit waves
                 else
                     wave_sync();
-                TRACE(1);
-
-                // ---- 2. exchange A: partial Ypred across groups ------------------
-                // lane: rows (ra, ra + 1), peers agi * APL + x; sums in group order
-                float y0 = 0.f, y1 = 0.f;
-                if constexpr (PX > 1) {
-                    const uint32_t bA = 8u * (uint32_t)((par * PR + gb) * PX * RMAX);
+                if constexpr (!DIRECT && PX > 1) {
                     if (wu == 0 && lane < NRW) {
                         float v = 0.f;
 #pragma unroll
                         for (int w = 0; w < WU; ++w) v += Ypart[w * R + wr * NRW + lane];
                         st1(rA, bA + 8u * (uint32_t)(gx * RMAX + wr * NRW + lane), pack(v, tag), true);
                     }
-                    asm volatile("" ::: "memory");
-                    W2 w[S::APL];
-                    const uint32_t src = bA + 8u * (uint32_t)(agi * S::APL * RMAX + ra);
-                    auto reload = [&](int x) { return ld2(rA, src + 8u * (uint32_t)(x * RMAX)); };
-#pragma unroll
-                    for (int x = 0; x < S::APL; ++x) w[x] = reload(x);
-                    wt.settle(w, tag, reload);
-#pragma unroll
-                    for (int x = 0; x < S::APL; ++x) {
-                        y0 += val_of(w[x].a);
-                        y1 += val_of(w[x].b);
-                    }
-                    if constexpr (S::AG >= 2) { y0 += __shfl_xor(y0, S::NPR, 64); y1 += __shfl_xor(y1, S::NPR, 64); }
-                    if constexpr (S::AG >= 4) { y0 += __shfl_xor(y0, 2 * S::NPR, 64); y1 += __shfl_xor(y1, 2 * S::NPR, 64); }
-                    if constexpr (S::AG >= 8) { y0 += __shfl_xor(y0, 4 * S::NPR, 64); y1 += __shfl_xor(y1, 4 * S::NPR, 64); }
-                } else {
-#pragma unroll
-                    for (int w = 0; w < WU; ++w) {
-                        y0 += Ypart[w * R + ra];
-                        y1 += Ypart[w * R + ra + 1];
-                    }
                 }
-                TRACE(2);
+                asm volatile("" ::: "memory");
+                TRACE(1);
 
-                // residual, dZ2 (eqs. 14-15), SSE of the wave's rows
-                {
-                    const float e0 = y0 - Yb[ra], e1 = y1 - Yb[ra + 1];
-                    const bool in0 = ra < rc, in1 = ra + 1 < rc;
-                    const float g0 = in0 ? scale * e0 : 0.0f, g1 = in1 ? scale * e1 : 0.0f;
-                    const bool mine = lane < S::NPR && wu == 0;
-                    const float r2 = mine ? (in0 ? e0 * e0 : 0.0f) + (in1 ? e1 * e1 : 0.0f) : 0.0f;
-                    const float sse = sum64(r2);
-                    if (lane == 0) SseW[wave] = sse;
-                    if (lane < S::NPR) *reinterpret_cast<float2 *>(Gw + wave * NRW + 2 * pr2) = make_float2(g0, g1);
-                    wave_sync();
+                // ---- 2. exchange A, residual and backward, one row tile at a time --
+                // lane: rows (2 pp, 2 pp + 1) of the tile from group peer; the group
+                // sums run as a butterfly over lane groups of 8 (a fixed order), so
+                // the backward of a tile overlaps the exchange of the next.
+                const int pp = lane & 7;
+                const int peer = (lane >> 3) % PX;
+                W2 wa[RTW];
+                if constexpr (PX > 1) {
+#pragma unroll
+                    for (int i = 0; i < RTW; ++i)
+                        wa[i] = ld2(rA, bA + 8u * (uint32_t)(peer * RMAX + wr * NRW + 16 * i + 2 * pp));
                 }
-
-                // ---- 3. backward: P = X^T (dZ2 (.) mask) -------------------------
                 f4 pacc[2][NUW];
 #pragma unroll
                 for (int kt = 0; kt < 2; ++kt)
 #pragma unroll
                     for (int u = 0; u < NUW; ++u) pacc[kt][u] = f4{0.f, 0.f, 0.f, 0.f};
+                float r2acc = 0.f;
 #pragma unroll
                 for (int i = 0; i < RTW; ++i) {
                     const int tile = wr * RTW + i;
+                    const int ra = tile * 16 + 2 * pp;   // first row of the lane's pair
+                    float y0 = 0.f, y1 = 0.f;
+                    if constexpr (PX > 1) {
+                        W2 one[1] = {wa[i]};
+                        wt.settle(one, tag, [&](int) {
+                            return ld2(rA, bA + 8u * (uint32_t)(peer * RMAX + ra));
+                        });
+                        y0 = val_of(one[0].a);
+                        y1 = val_of(one[0].b);
+                        if constexpr (PX >= 2) { y0 += __shfl_xor(y0, 8, 64); y1 += __shfl_xor(y1, 8, 64); }
+                        if constexpr (PX >= 4) { y0 += __shfl_xor(y0, 16, 64); y1 += __shfl_xor(y1, 16, 64); }
+                        if constexpr (PX >= 8) { y0 += __shfl_xor(y0, 32, 64); y1 += __shfl_xor(y1, 32, 64); }
+                    } else {
+#pragma unroll
+                        for (int w = 0; w < WU; ++w) {
+                            y0 += Ypart[w * R + ra];
+                            y1 += Ypart[w * R + ra + 1];
+                        }
+                    }
+                    // residual, dZ2 (eqs. 14-15), squared residuals
+                    {
+                        const float e0 = y0 - Yb[ra], e1 = y1 - Yb[ra + 1];
+                        const bool in0 = ra < rc, in1 = ra + 1 < rc;
+                        const float g0 = in0 ? scale * e0 : 0.0f, g1 = in1 ? scale * e1 : 0.0f;
+                        if (lane < 8 && wu == 0) r2acc += (in0 ? e0 * e0 : 0.0f) + (in1 ? e1 * e1 : 0.0f);
+                        if (lane < 8) *reinterpret_cast<float2 *>(Gw + wave * NRW + 16 * i + 2 * pp) = make_float2(g0, g1);
+                        wave_sync();
+                    }
+                    if (i == 0) TRACE(2);
+                    // ---- 3. backward: P += X_tile^T (dZ2 (.) mask) ----------------
                     const float4 g4 = *reinterpret_cast<const float4 *>(Gw + wave * NRW + 16 * i + 4 * lq);
                     const float gv[4] = {g4.x, g4.y, g4.z, g4.w};
 #pragma unroll
@@ -585,6 +590,10 @@ __global__ __launch_bounds__(NTHR) void k_train(const TrainArgs a) {
                             pacc[1][u] = __builtin_amdgcn_mfma_f32_16x16x4f32(xt1, gm, pacc[1][u], 0, 0, 0);
                         }
                     }
+                }
+                {
+                    const float sse = sum64(r2acc);
+                    if (lane == 0) SseW[wave] = sse;
                 }
 #pragma unroll
                 for (int kt = 0; kt < 2; ++kt)
