@@ -6,8 +6,9 @@
 //     on one XCD (8 XCDs, one L2 each) and owns U = h/PX units;
 //   - inside a group, PR workgroups split the rows of every mini-batch (R rows
 //     each); every workgroup holds the group's W1 slice [32 x U] and W2 slice [U].
-// A workgroup has four compute waves (one per SIMD, all on MFMA) and one loader
-// wave that gathers the rows of later steps through the epoch permutation.
+// A workgroup has four compute waves (one per SIMD, all on MFMA) and two loader
+// waves that gather the rows of later steps through the epoch permutation (one
+// loader wave alone is limited by how fast it can issue the gathers).
 // One SGD step is:
 //   1. Z1 = X W1 on fp32 MFMA (16x16x4) from the rows staged in LDS; ReLU mask
 //      bits and the partial Ypred over the group's units stay in registers
@@ -53,7 +54,8 @@ namespace mlp {
 typedef float f4 __attribute__((ext_vector_type(4)));
 
 constexpr int NCW = 4;                  // compute waves per workgroup
-constexpr int NTHR = 64 * (NCW + 1);    // plus one loader wave
+constexpr int NLW = 2;                  // loader waves
+constexpr int NTHR = 64 * (NCW + NLW);  // threads per workgroup
 
 // ---------------------------------------------------------------------------
 // Shapes
@@ -84,7 +86,7 @@ struct Shape {
     static constexpr int PS = U + 1;                       // P partial row stride
     static constexpr int RSW = 32 * U;                     // exchange-B words per workgroup
     static constexpr int GBW = (PR * RSW + PR + 31) / 32 * 32;   // exchange-B words per group
-    static constexpr int RPL = R / 8;                      // rows per loader lane
+    static constexpr int RPL = R / (8 * NLW);              // rows per loader lane
     // LDS carve-up, in floats
     static constexpr int O_X = 0;                          // [2][R][XS] staged rows
     static constexpr int O_Y = O_X + 2 * R * XS;           // [2][R]
@@ -311,7 +313,7 @@ constexpr int TRACE_ALL_FIRST = 16, TRACE_ALL_STEPS = 8;
 // The kernel
 // ---------------------------------------------------------------------------
 // Compute wave w = wr + wu * WR takes row tiles [wr * RTW, (wr + 1) * RTW) and
-// unit tiles {wu + i * WU}. Wave NCW is the loader. Both kinds of wave pass the
+// unit tiles {wu + i * WU}. Waves NCW.. are the loaders. Both kinds of wave pass the
 // same workgroup barriers: one before the loop, then per step [one more when
 // WU > 1,] "P partials ready" and "next step ready".
 template <class S, bool TR>
@@ -759,11 +761,12 @@ __global__ __launch_bounds__(NTHR) void k_train(const TrainArgs a) {
                 if (k0 == 0) COLD(W2)[ug] = ow2;
             }
         } else {
-            // ================= loader wave ====================================
+            // ================= loader waves ===================================
+            // loader wave l takes rows {8 l + r8 + 16 j}
             // Indices are loaded two steps ahead and rows one step ahead into
             // registers; a step's rows are written to LDS during the step before.
             constexpr int RPL = S::RPL;
-            const int lc = lane & 7, lr0 = lane >> 3;   // float4 chunk, first row
+            const int lc = lane & 7, lr0 = (lane >> 3) + 8 * (wave - NCW);   // float4 chunk, first row
             const int64_t row0 = (int64_t)gb * R;
             int32_t pidx[RPL];
             float4 pfx[RPL];
@@ -774,7 +777,7 @@ __global__ __launch_bounds__(NTHR) void k_train(const TrainArgs a) {
                 const int64_t n = COLD(n);
 #pragma unroll
                 for (int j = 0; j < RPL; ++j) {
-                    int64_t pos = off + row0 + lr0 + 8 * j;
+                    int64_t pos = off + row0 + lr0 + 8 * NLW * j;
                     if (perm) {
                         pos = pos < n ? pos : n - 1;                // always a valid address
                         pidx[j] = perm[(int64_t)ps.e * n + pos];
@@ -790,7 +793,7 @@ __global__ __launch_bounds__(NTHR) void k_train(const TrainArgs a) {
                 const int64_t n_rows = COLD(n_rows);
 #pragma unroll
                 for (int j = 0; j < RPL; ++j) {
-                    const int r = lr0 + 8 * j;
+                    const int r = lr0 + 8 * NLW * j;
                     float4 v = make_float4(0.f, 0.f, 0.f, 0.f);
                     float y = 0.f;
                     if (r < rcl) {
@@ -812,7 +815,7 @@ __global__ __launch_bounds__(NTHR) void k_train(const TrainArgs a) {
                 float *Yd = Yall + buf * R;
 #pragma unroll
                 for (int j = 0; j < RPL; ++j) {
-                    const int r = lr0 + 8 * j;
+                    const int r = lr0 + 8 * NLW * j;
                     *reinterpret_cast<float4 *>(Xd + r * XS + 4 * lc) = pfx[j];
                     if (lc == 0) Yd[r] = pfy[j];
                 }
