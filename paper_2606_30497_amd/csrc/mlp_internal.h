@@ -43,6 +43,7 @@ struct TrainPlan {
     int rs_stride = 0;  // words per workgroup in the exchange-B buffer
     int grid = 0;       // workgroups launched (8 * pr)
     size_t lds = 0;     // dynamic LDS bytes
+    double cost = 0.0;  // modelled seconds per step
 };
 
 struct TrainArgs {

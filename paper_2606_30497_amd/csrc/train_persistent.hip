@@ -888,6 +888,23 @@ static hipError_t launch_shape(hipStream_t stream, TrainArgs &a) {
                                       stream);
 }
 
+// Modelled step time (seconds): MFMA work of one wave (forward and backward, 32
+// cycles per 16x16x4 fp32 MFMA at 2.4 GHz), exchange A across XCDs when PX > 1,
+// the rounds of exchanges B and C (each round one load round trip) and the
+// owner's loads per lane. The constants are fitted to step times measured on
+// MI355X (at batch 64 and 256, eight groups of few workgroups beat one group of
+// many or four groups).
+template <class S>
+static double shape_cost() {
+    constexpr int CHB = S::LPS < 8 ? S::LPS : 8;
+    constexpr int rounds_b = S::LPS / CHB;
+    constexpr int NP = S::U * 33 / 2, FULL = NP / 256, CH = FULL < 9 ? FULL : 8;
+    constexpr int rounds_c = (FULL + CH - 1) / CH;
+    const double compute = 32.0 * 16.0 * S::NUW * S::RTW / 2.4e9;
+    return compute + (S::PX > 1 ? 1.5e-6 : 0.0) + 0.6e-6 * rounds_b + 0.05e-6 * S::LPS +
+           0.5e-6 * rounds_c;
+}
+
 template <class S>
 static TrainPlan plan_of(int inst) {
     TrainPlan p;
@@ -907,6 +924,7 @@ static TrainPlan plan_of(int inst) {
     const size_t bytes = sizeof(float) * (size_t)S::LDS_FLOATS;
     const size_t one_per_cu = 84 * 1024;   // > half of the 160 KB LDS: one workgroup per CU
     p.lds = bytes > one_per_cu ? bytes : one_per_cu;
+    p.cost = shape_cost<S>();
     return p;
 }
 
@@ -925,7 +943,10 @@ static TrainPlan plan_of(int inst) {
     X(9, 1, 16, 16, 64)    /* 32-64-1,   batch <= 256, one XCD */     \
     X(10, 1, 8, 32, 32)    /* 32-32-1,   batch <= 256, one XCD */     \
     X(11, 4, 16, 16, 64)   /* 32-256-1,  batch <= 256, four XCDs */   \
-    X(12, 2, 16, 16, 128)  /* 32-256-1,  batch <= 256, two XCDs */
+    X(12, 2, 16, 16, 128)  /* 32-256-1,  batch <= 256, two XCDs */    \
+    X(13, 4, 4, 16, 64)    /* 32-256-1,  batch <= 64,  four XCDs */   \
+    X(14, 8, 4, 32, 32)    /* 32-256-1,  batch <= 128 */              \
+    X(15, 8, 8, 32, 32)    /* 32-256-1,  batch <= 256 */
 
 #define MLP_SHAPE_TYPE(I, PX, PR, R, U) typedef Shape<PX, PR, R, U> Shape##I;
 MLP_SHAPES(MLP_SHAPE_TYPE)
@@ -941,15 +962,6 @@ static const TrainPlan *all_plans(int *count) {
     }
     *count = n;
     return plans;
-}
-
-// Modelled step time: MFMA work of one wave (forward and backward, 32 cycles
-// per 16x16x4 fp32 MFMA) plus the exchange latencies (one across XCDs when
-// PX > 1, two inside one XCD).
-static double plan_cost(const TrainPlan &pl) {
-    const double mfma_cycles = 32.0 * 16.0 * pl.nuw * pl.rtw;
-    const double compute = mfma_cycles / 2.4e9;
-    return compute + (pl.px > 1 ? 1.5e-6 : 0.0) + 1.4e-6;
 }
 
 bool plan_train(int hidden, int64_t batch, TrainPlan *plan) {
@@ -969,7 +981,7 @@ bool plan_train(int hidden, int64_t batch, TrainPlan *plan) {
         if (fpx && pl.px != fpx) continue;
         if (finst >= 0 && pl.inst != finst) continue;
         // modelled cost first, then the tightest capacity (fewest idle rows)
-        const double cst = plan_cost(pl);
+        const double cst = pl.cost;
         if (!found || cst < best_cost - 1e-12 || (cst < best_cost + 1e-12 && cap < best_cap)) {
             *plan = pl;
             best_cost = cst;

@@ -305,7 +305,8 @@ def _env(**kv):
 FUSED_SHAPES = [(8, 32, 128, 32), (8, 32, 64, 32), (8, 32, 32, 32), (4, 32, 16, 64),
                 (1, 16, 16, 256), (8, 32, 32, 128), (8, 32, 16, 128),
                 (8, 32, 16, 64), (2, 16, 16, 64), (1, 16, 16, 64), (1, 8, 32, 32),
-                (4, 16, 16, 64), (2, 16, 16, 128)]
+                (4, 16, 16, 64), (2, 16, 16, 128), (4, 4, 16, 64), (8, 4, 32, 32),
+                (8, 8, 32, 32)]
 # Index = position in the library's shape table. A one-XCD shape with four
 # workgroups of 64 owned units each, (1, 4, 16, 256), is disabled: its
 # gradient sums came out wrong from the second SGD step on, and one run of it
