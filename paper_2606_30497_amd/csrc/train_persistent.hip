@@ -102,7 +102,7 @@ struct Shape {
     static_assert(NUW >= 1 && RTW >= 1 && NUW * RTW <= 8, "mask bits");
     static_assert(NRW == 16 || NRW == 32 || NRW == 64, "exchange-A lanes");
     static_assert(U % PR == 0 && UPW >= 1, "units per workgroup");
-    static_assert(RSW % 256 == 0, "exchange-B stores");
+    static_assert(RSW % 512 == 0, "exchange-B stores");
     static_assert(R <= RMAX && R <= 128, "rows");
     static_assert(PX == 1 || PX == 2 || PX == 4 || PX == 8, "groups");
     static_assert(PR >= 1 && PR <= 32, "workgroups per group");
@@ -160,6 +160,16 @@ __device__ __forceinline__ void st1(rsrc_t r, uint32_t off, uint64_t w, bool dev
         __builtin_amdgcn_raw_buffer_store_b64(v, r, off, 0, CPOL_SC1);
     else
         __builtin_amdgcn_raw_buffer_store_b64(v, r, off, 0, 0);
+}
+// store of two adjacent words (16-byte aligned) in one 16-byte store; a reader
+// checks the tag of each 8-byte word on its own
+__device__ __forceinline__ void st2(rsrc_t r, uint32_t off, uint64_t w0, uint64_t w1, bool dev) {
+    const i4v v = {(int)(uint32_t)w0, (int)(uint32_t)(w0 >> 32), (int)(uint32_t)w1,
+                   (int)(uint32_t)(w1 >> 32)};
+    if (dev)
+        __builtin_amdgcn_raw_buffer_store_b128(v, r, off, 0, CPOL_SC1);
+    else
+        __builtin_amdgcn_raw_buffer_store_b128(v, r, off, 0, 0);
 }
 __device__ __forceinline__ uint32_t stale(uint64_t w, uint32_t tag) { return tag_of(w) ^ tag; }
 __device__ __forceinline__ uint32_t stale(const W2 &w, uint32_t tag) {
@@ -222,7 +232,6 @@ struct Waiter {
                 check(deadline);
                 if (aborted) break;
             }
-            __builtin_amdgcn_s_sleep(1);
             asm volatile("" ::: "memory");   // the reloads are not the loads above
 #pragma unroll
             for (int i = 0; i < N; ++i) w[i] = reload(i);
@@ -628,14 +637,18 @@ __global__ __launch_bounds__(NTHR) void k_train(const TrainArgs a) {
                 // word (ul, k) of this workgroup goes to owner o = ul / UPW at word
                 // (o * PR + gb) * NPAIR + (ul % UPW) * 32 + k of the group block
 #pragma unroll
-                for (int i0 = 0; i0 < S::RSW; i0 += 256) {
-                    const int i = i0 + tid;
+                for (int i0 = 0; i0 < S::RSW; i0 += 512) {
+                    const int i = i0 + 2 * tid;          // words i, i + 1: k even
                     const int ul = i >> 5, k = i & 31;
-                    float v = 0.f;
+                    float v0 = 0.f, v1 = 0.f;
 #pragma unroll
-                    for (int w = 0; w < WR; ++w) v += Pred[(w * 32 + k) * PS + ul];
+                    for (int w = 0; w < WR; ++w) {
+                        v0 += Pred[(w * 32 + k) * PS + ul];
+                        v1 += Pred[(w * 32 + k + 1) * PS + ul];
+                    }
                     const int o = ul / UPW, jo = ul - o * UPW;
-                    st1(rB, bB + 8u * (uint32_t)((o * PR + gb) * NPAIR + jo * 32 + k), pack(v, tag), !plain);
+                    st2(rB, bB + 8u * (uint32_t)((o * PR + gb) * NPAIR + jo * 32 + k), pack(v0, tag),
+                        pack(v1, tag), !plain);
                 }
                 if (tid == 0) {
                     float v = 0.f;
