@@ -508,15 +508,22 @@ __global__ __launch_bounds__(NTHR) void k_train(const TrainArgs a) {
                             mbits |= (on ? 1u : 0u) << ((i * NUW + u) * 4 + v);
                             yp[v] = fmaf(on ? z : 0.0f, w2v[u], yp[v]);     // eqs. 12-13
                         }
+                    if constexpr (DIRECT) {
+                        // lane 15 of row group g holds rows 4 g + v; bring row l of the
+                        // tile to lane l (l < 16) and store the tile's 16 words at once
+                        float rowv = 0.f;
 #pragma unroll
-                    for (int v = 0; v < 4; ++v) {
-                        const float sv = row16_sum(yp[v]);
-                        if (li == 15) {
-                            const int row = tile * 16 + 4 * lq + v;
-                            if constexpr (DIRECT)
-                                st1(rA, bA + 8u * (uint32_t)(gx * RMAX + row), pack(sv, tag), true);
-                            else
-                                Ypart[wu * R + row] = sv;
+                        for (int v = 0; v < 4; ++v) {
+                            const float t = __shfl(row16_sum(yp[v]), 16 * ((lane >> 2) & 3) + 15, 64);
+                            rowv = (lane & 3) == v ? t : rowv;
+                        }
+                        if (lane < 16)
+                            st1(rA, bA + 8u * (uint32_t)(gx * RMAX + tile * 16 + lane), pack(rowv, tag), true);
+                    } else {
+#pragma unroll
+                        for (int v = 0; v < 4; ++v) {
+                            const float sv = row16_sum(yp[v]);
+                            if (li == 15) Ypart[wu * R + tile * 16 + 4 * lq + v] = sv;
                         }
                     }
                 }
