@@ -517,8 +517,12 @@ __global__ __launch_bounds__(NTHR) void k_train(const TrainArgs a) {
                             const float t = __shfl(row16_sum(yp[v]), 16 * ((lane >> 2) & 3) + 15, 64);
                             rowv = (lane & 3) == v ? t : rowv;
                         }
-                        if (lane < 16)
-                            st1(rA, bA + 8u * (uint32_t)(gx * RMAX + tile * 16 + lane), pack(rowv, tag), true);
+                        // group 0 folds -Y into its partial, so the group sum is the
+                        // residual Ypred - Y and the other groups need no targets
+                        if (lane < 16) {
+                            const float yv = gx == 0 ? Yb[tile * 16 + lane] : 0.0f;
+                            st1(rA, bA + 8u * (uint32_t)(gx * RMAX + tile * 16 + lane), pack(rowv - yv, tag), true);
+                        }
                     } else {
 #pragma unroll
                         for (int v = 0; v < 4; ++v) {
@@ -537,6 +541,7 @@ __global__ __launch_bounds__(NTHR) void k_train(const TrainArgs a) {
                         float v = 0.f;
 #pragma unroll
                         for (int w = 0; w < WU; ++w) v += Ypart[w * R + wr * NRW + lane];
+                        if (gx == 0) v -= Yb[wr * NRW + lane];   // residual, as above
                         st1(rA, bA + 8u * (uint32_t)(gx * RMAX + wr * NRW + lane), pack(v, tag), true);
                     }
                 }
@@ -585,7 +590,8 @@ __global__ __launch_bounds__(NTHR) void k_train(const TrainArgs a) {
                     }
                     // residual, dZ2 (eqs. 14-15), squared residuals
                     {
-                        const float e0 = y0 - Yb[ra], e1 = y1 - Yb[ra + 1];
+                        // across groups the exchanged sum is already Ypred - Y
+                        const float e0 = PX > 1 ? y0 : y0 - Yb[ra], e1 = PX > 1 ? y1 : y1 - Yb[ra + 1];
                         const bool in0 = ra < rc, in1 = ra + 1 < rc;
                         const float g0 = in0 ? scale * e0 : 0.0f, g1 = in1 ? scale * e1 : 0.0f;
                         if (lane < 8 && wu == 0) r2acc += (in0 ? e0 * e0 : 0.0f) + (in1 ? e1 * e1 : 0.0f);
@@ -788,6 +794,7 @@ __global__ __launch_bounds__(NTHR) void k_train(const TrainArgs a) {
             constexpr int RPL = S::RPL;
             const int lc = lane & 7, lr0 = (lane >> 3) + 8 * (wave - NCW);   // float4 chunk, first row
             const int64_t row0 = (int64_t)gb * R;
+            const bool needy = PX == 1 || gx == 0;   // only group 0 uses the targets
             int32_t pidx[RPL];
             float4 pfx[RPL];
             float pfy[RPL];
@@ -824,7 +831,7 @@ __global__ __launch_bounds__(NTHR) void k_train(const TrainArgs a) {
                             row = 0;
                         }
                         v = *reinterpret_cast<const float4 *>(X + row * D_IN + 4 * lc);
-                        if (lc == 0) y = Y[row];
+                        if (lc == 0 && needy) y = Y[row];
                     }
                     pfx[j] = v;
                     pfy[j] = y;
