@@ -798,22 +798,24 @@ __global__ __launch_bounds__(NTHR) void k_train(const TrainArgs a) {
             int32_t pidx[RPL];
             float4 pfx[RPL];
             float pfy[RPL];
+            // indices of a step: one load, lane m (m < R/2) holding row
+            // 8 l + m % 8 + 16 (m / 8) of loader wave l; spread to the row lanes
+            // when the rows are fetched
+            int32_t cidx = 0;
             auto fetch_idx = [&](const Pos &ps) {
                 const int64_t off = (int64_t)ps.sb * COLD(batch);
                 const int32_t *perm = COLD(perm);
                 const int64_t n = COLD(n);
-#pragma unroll
-                for (int j = 0; j < RPL; ++j) {
-                    int64_t pos = off + row0 + lr0 + 8 * NLW * j;
-                    if (perm) {
-                        pos = pos < n ? pos : n - 1;                // always a valid address
-                        pidx[j] = perm[(int64_t)ps.e * n + pos];
-                    } else {
-                        pidx[j] = (int32_t)pos;
-                    }
-                }
+                const int m = lane < R / 2 ? lane : 0;
+                const int64_t pos = off + row0 + 8 * (wave - NCW) + (m & 7) + 16 * (m >> 3);
+                if (perm)
+                    cidx = perm[(int64_t)ps.e * n + (pos < n ? pos : n - 1)];   // always a valid address
+                else
+                    cidx = (int32_t)pos;
             };
             auto fetch_rows = [&](const Pos &ps) {
+#pragma unroll
+                for (int j = 0; j < RPL; ++j) pidx[j] = __shfl(cidx, 8 * j + (lane >> 3), 64);
                 const int nbr = ps.sb == spe - 1 ? tail : batch;
                 const int64_t rcl = nbr - row0;
                 const float *X = COLD(X), *Y = COLD(Y);
