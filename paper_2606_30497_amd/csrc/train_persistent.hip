@@ -259,36 +259,36 @@ __device__ __forceinline__ void gather_slice(Waiter &wt, rsrc_t r, uint32_t base
     }
 }
 
-// Sum over each row of 16 lanes by DPP right shifts (bound_ctrl: lanes shifted
-// in from outside the row read 0); lane 15 of the row holds the total, summed
-// in a fixed order.
-__device__ __forceinline__ float row16_sum(float v) {
-    v += __builtin_bit_cast(float, __builtin_amdgcn_update_dpp(0, __builtin_bit_cast(int, v), 0x111, 0xF, 0xF, true));
-    v += __builtin_bit_cast(float, __builtin_amdgcn_update_dpp(0, __builtin_bit_cast(int, v), 0x112, 0xF, 0xF, true));
-    v += __builtin_bit_cast(float, __builtin_amdgcn_update_dpp(0, __builtin_bit_cast(int, v), 0x114, 0xF, 0xF, true));
-    v += __builtin_bit_cast(float, __builtin_amdgcn_update_dpp(0, __builtin_bit_cast(int, v), 0x118, 0xF, 0xF, true));
+// Cross-lane sums on the VALU (DPP and lane-swap instructions, no LDS round
+// trips). Each pairs lanes symmetrically, so both lanes of a pair compute the
+// same sum bitwise (a + b == b + a): every lane of a group ends with the same
+// total, summed in a fixed order.
+template <int CTRL>
+__device__ __forceinline__ float dppf(float v) {
+    return __builtin_bit_cast(float, __builtin_amdgcn_update_dpp(0, __builtin_bit_cast(int, v), CTRL, 0xF, 0xF, false));
+}
+// v + (v of lane l ^ 8), within each row of 16 lanes (row_ror:8)
+__device__ __forceinline__ float xadd8(float v) { return v + dppf<0x128>(v); }
+// v + (v of lane l ^ 16)
+__device__ __forceinline__ float xadd16(float v) {
+    const auto r = __builtin_amdgcn_permlane16_swap(__float_as_uint(v), __float_as_uint(v), false, false);
+    return __uint_as_float(r[0]) + __uint_as_float(r[1]);
+}
+// v + (v of lane l ^ 32)
+__device__ __forceinline__ float xadd32(float v) {
+    const auto r = __builtin_amdgcn_permlane32_swap(__float_as_uint(v), __float_as_uint(v), false, false);
+    return __uint_as_float(r[0]) + __uint_as_float(r[1]);
+}
+// sum over each row of 16 lanes, in every lane of the row: pairs (i, i^8),
+// (i, 7-i within 8), (i, i^2), (i, i^1)
+__device__ __forceinline__ float rsum16(float v) {
+    v += dppf<0x128>(v);   // row_ror:8
+    v += dppf<0x141>(v);   // row_half_mirror
+    v += dppf<0x4E>(v);    // quad_perm [2,3,0,1]
+    v += dppf<0xB1>(v);    // quad_perm [1,0,3,2]
     return v;
 }
-// Butterfly sums (every lane gets the total, in a fixed order).
-__device__ __forceinline__ float sum32(float v) {
-    v += __shfl_xor(v, 16, 64);
-    v += __shfl_xor(v, 8, 64);
-    v += __shfl_xor(v, 4, 64);
-    v += __shfl_xor(v, 2, 64);
-    v += __shfl_xor(v, 1, 64);
-    return v;
-}
-__device__ __forceinline__ float sum16(float v) {
-    v += __shfl_xor(v, 8, 64);
-    v += __shfl_xor(v, 4, 64);
-    v += __shfl_xor(v, 2, 64);
-    v += __shfl_xor(v, 1, 64);
-    return v;
-}
-__device__ __forceinline__ float sum64(float v) {
-    v = sum32(v);
-    return v + __shfl_xor(v, 32, 64);
-}
+__device__ __forceinline__ float sum64(float v) { return xadd32(xadd16(rsum16(v))); }
 
 // (epoch, step within the epoch) of a step
 struct Pos {
@@ -509,25 +509,27 @@ __global__ __launch_bounds__(NTHR) void k_train(const TrainArgs a) {
                             yp[v] = fmaf(on ? z : 0.0f, w2v[u], yp[v]);     // eqs. 12-13
                         }
                     if constexpr (DIRECT) {
-                        // lane 15 of row group g holds rows 4 g + v; bring row l of the
-                        // tile to lane l (l < 16) and store the tile's 16 words at once
+                        // every lane of row group g gets the sums of rows 4 g + v;
+                        // lanes with li < 4 store row 4 g + li, so the tile's 16 words
+                        // go out in one store
                         float rowv = 0.f;
 #pragma unroll
                         for (int v = 0; v < 4; ++v) {
-                            const float t = __shfl(row16_sum(yp[v]), 16 * ((lane >> 2) & 3) + 15, 64);
-                            rowv = (lane & 3) == v ? t : rowv;
+                            const float t = rsum16(yp[v]);
+                            rowv = li == v ? t : rowv;
                         }
                         // group 0 folds -Y into its partial, so the group sum is the
                         // residual Ypred - Y and the other groups need no targets
-                        if (lane < 16) {
-                            const float yv = gx == 0 ? Yb[tile * 16 + lane] : 0.0f;
-                            st1(rA, bA + 8u * (uint32_t)(gx * RMAX + tile * 16 + lane), pack(rowv - yv, tag), true);
+                        if (li < 4) {
+                            const int row = tile * 16 + 4 * lq + li;
+                            const float yv = gx == 0 ? Yb[row] : 0.0f;
+                            st1(rA, bA + 8u * (uint32_t)(gx * RMAX + row), pack(rowv - yv, tag), true);
                         }
                     } else {
 #pragma unroll
                         for (int v = 0; v < 4; ++v) {
-                            const float sv = row16_sum(yp[v]);
-                            if (li == 15) Ypart[wu * R + tile * 16 + 4 * lq + v] = sv;
+                            const float sv = rsum16(yp[v]);
+                            if (li == 0) Ypart[wu * R + tile * 16 + 4 * lq + v] = sv;
                         }
                     }
                 }
@@ -578,9 +580,9 @@ __global__ __launch_bounds__(NTHR) void k_train(const TrainArgs a) {
                         });
                         y0 = val_of(one[0].a);
                         y1 = val_of(one[0].b);
-                        if constexpr (PX >= 2) { y0 += __shfl_xor(y0, 8, 64); y1 += __shfl_xor(y1, 8, 64); }
-                        if constexpr (PX >= 4) { y0 += __shfl_xor(y0, 16, 64); y1 += __shfl_xor(y1, 16, 64); }
-                        if constexpr (PX >= 8) { y0 += __shfl_xor(y0, 32, 64); y1 += __shfl_xor(y1, 32, 64); }
+                        if constexpr (PX >= 2) { y0 = xadd8(y0); y1 = xadd8(y1); }
+                        if constexpr (PX >= 4) { y0 = xadd16(y0); y1 = xadd16(y1); }
+                        if constexpr (PX >= 8) { y0 = xadd32(y0); y1 = xadd32(y1); }
                     } else {
 #pragma unroll
                         for (int w = 0; w < WU; ++w) {
@@ -691,12 +693,17 @@ __global__ __launch_bounds__(NTHR) void k_train(const TrainArgs a) {
                             p1 += val_of(w[b].b);
                         }
                     }
-                    if constexpr (SG >= 2) { p0 += __shfl_xor(p0, KPW, 64); p1 += __shfl_xor(p1, KPW, 64); }
-                    if constexpr (SG >= 4) { p0 += __shfl_xor(p0, 2 * KPW, 64); p1 += __shfl_xor(p1, 2 * KPW, 64); }
+                    if constexpr (SG == 4) {   // lane groups of 16
+                        p0 = xadd32(xadd16(p0));
+                        p1 = xadd32(xadd16(p1));
+                    } else if constexpr (SG == 2) {   // lane groups of 32
+                        p0 = xadd32(p0);
+                        p1 = xadd32(p1);
+                    }
                     TRACE_BY(4, OW0 * 64);
                     // ---- update the owned units (eq. 19) or emit gradients ------
                     const float dw1a = ow2 * p0, dw1b = ow2 * p1;       // dW1_kj = W2_j P_kj
-                    const float dw2 = sum16(fmaf(ow1b, p1, ow1a * p0)); // dW2_j = sum_k W1_kj P_kj
+                    const float dw2 = rsum16(fmaf(ow1b, p1, ow1a * p0)); // dW2_j = sum_k W1_kj P_kj
                     if (a.mode == 1) {
                         if (sg == 0) {
                             float *dW1 = COLD(dW1);
