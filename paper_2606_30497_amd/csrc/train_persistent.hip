@@ -91,8 +91,7 @@ struct Shape {
     static constexpr int O_X = 0;                          // [2][R][XS] staged rows
     static constexpr int O_Y = O_X + 2 * R * XS;           // [2][R]
     static constexpr int O_YP = O_Y + 2 * R;               // [WU][R] partial Ypred
-    static constexpr int O_G = O_YP + WU * R;              // [NCW][NRW] dZ2 per wave
-    static constexpr int O_P = O_G + NCW * NRW;            // [WR][32][PS] P partials
+    static constexpr int O_P = O_YP + WU * R;              // [WR][32][PS] P partials
     static constexpr int O_WSL = O_P + WR * 32 * PS;       // [U][WS] weight slice
     static constexpr int O_SSE = O_WSL + U * WS;           // [NCW]
     static constexpr int LDS_FLOATS = O_SSE + NCW;
@@ -106,7 +105,7 @@ struct Shape {
     static_assert(R <= RMAX && R <= 128, "rows");
     static_assert(PX == 1 || PX == 2 || PX == 4 || PX == 8, "groups");
     static_assert(PR >= 1 && PR <= 32, "workgroups per group");
-    static_assert(O_WSL % 4 == 0 && O_G % 4 == 0, "float4 alignment");
+    static_assert(O_WSL % 4 == 0, "float4 alignment");
 };
 
 // ---------------------------------------------------------------------------
@@ -395,7 +394,6 @@ __global__ __launch_bounds__(NTHR) void k_train(const TrainArgs a) {
     float *Xall = lds + S::O_X;     // [2][R][XS]
     float *Yall = lds + S::O_Y;     // [2][R]
     float *Ypart = lds + S::O_YP;   // [WU][R]
-    float *Gw = lds + S::O_G;       // [NCW][NRW]
     float *Pred = lds + S::O_P;     // [WR][32][PS]
     float *Wsl = lds + S::O_WSL;    // [U][WS]
     float *SseW = lds + S::O_SSE;   // [NCW]
@@ -551,16 +549,19 @@ __global__ __launch_bounds__(NTHR) void k_train(const TrainArgs a) {
                 TRACE(1);
 
                 // ---- 2. exchange A, residual and backward, one row tile at a time --
-                // lane: rows (2 pp, 2 pp + 1) of the tile from group peer; the group
-                // sums run as a butterfly over lane groups of 8 (a fixed order), so
-                // the backward of a tile overlaps the exchange of the next.
-                const int pp = lane & 7;
-                const int peer = (lane >> 3) % PX;
+                // lane (lq, li): rows 4 lq + 2 h, 4 lq + 2 h + 1 (h = li >> 3) of the
+                // tile from group peer li & 7; the group sums run as a symmetric
+                // butterfly over the 8 lanes of a half-row (a fixed order), and the
+                // other half-row supplies the lane's other two rows, so each lane
+                // ends with dZ2 of exactly the rows its backward MFMA operands need.
+                // The backward of a tile overlaps the exchange of the next.
+                const int hh = li >> 3;
+                const int peer = (li & 7) % PX;
                 W2 wa[RTW];
                 if constexpr (PX > 1) {
 #pragma unroll
                     for (int i = 0; i < RTW; ++i)
-                        wa[i] = ld2(rA, bA + 8u * (uint32_t)(peer * RMAX + wr * NRW + 16 * i + 2 * pp));
+                        wa[i] = ld2(rA, bA + 8u * (uint32_t)(peer * RMAX + (wr * RTW + i) * 16 + 4 * lq + 2 * hh));
                 }
                 f4 pacc[2][NUW];
 #pragma unroll
@@ -571,7 +572,7 @@ __global__ __launch_bounds__(NTHR) void k_train(const TrainArgs a) {
 #pragma unroll
                 for (int i = 0; i < RTW; ++i) {
                     const int tile = wr * RTW + i;
-                    const int ra = tile * 16 + 2 * pp;   // first row of the lane's pair
+                    const int ra = tile * 16 + 4 * lq + 2 * hh;   // first row of the lane's pair
                     float y0 = 0.f, y1 = 0.f;
                     if constexpr (PX > 1) {
                         W2 one[1] = {wa[i]};
@@ -580,9 +581,16 @@ __global__ __launch_bounds__(NTHR) void k_train(const TrainArgs a) {
                         });
                         y0 = val_of(one[0].a);
                         y1 = val_of(one[0].b);
-                        if constexpr (PX >= 2) { y0 = xadd8(y0); y1 = xadd8(y1); }
-                        if constexpr (PX >= 4) { y0 = xadd16(y0); y1 = xadd16(y1); }
-                        if constexpr (PX >= 8) { y0 = xadd32(y0); y1 = xadd32(y1); }
+                        if constexpr (PX == 8) {
+                            y0 += dppf<0x141>(y0);   // row_half_mirror: lanes i, 7 - i
+                            y1 += dppf<0x141>(y1);
+                        }
+                        if constexpr (PX >= 4) {
+                            y0 += dppf<0x4E>(y0);    // lanes i, i ^ 2
+                            y1 += dppf<0x4E>(y1);
+                        }
+                        y0 += dppf<0xB1>(y0);        // lanes i, i ^ 1
+                        y1 += dppf<0xB1>(y1);
                     } else {
 #pragma unroll
                         for (int w = 0; w < WU; ++w) {
@@ -591,19 +599,21 @@ __global__ __launch_bounds__(NTHR) void k_train(const TrainArgs a) {
                         }
                     }
                     // residual, dZ2 (eqs. 14-15), squared residuals
+                    float gv[4];
                     {
                         // across groups the exchanged sum is already Ypred - Y
                         const float e0 = PX > 1 ? y0 : y0 - Yb[ra], e1 = PX > 1 ? y1 : y1 - Yb[ra + 1];
                         const bool in0 = ra < rc, in1 = ra + 1 < rc;
                         const float g0 = in0 ? scale * e0 : 0.0f, g1 = in1 ? scale * e1 : 0.0f;
-                        if (lane < 8 && wu == 0) r2acc += (in0 ? e0 * e0 : 0.0f) + (in1 ? e1 * e1 : 0.0f);
-                        if (lane < 8) *reinterpret_cast<float2 *>(Gw + wave * NRW + 16 * i + 2 * pp) = make_float2(g0, g1);
-                        wave_sync();
+                        if ((li & 7) == 0 && wu == 0) r2acc += (in0 ? e0 * e0 : 0.0f) + (in1 ? e1 * e1 : 0.0f);
+                        const float o0 = dppf<0x128>(g0), o1 = dppf<0x128>(g1);   // lane li ^ 8
+                        gv[0] = hh ? o0 : g0;
+                        gv[1] = hh ? o1 : g1;
+                        gv[2] = hh ? g0 : o0;
+                        gv[3] = hh ? g1 : o1;
                     }
                     if (i == 0) TRACE(2);
                     // ---- 3. backward: P += X_tile^T (dZ2 (.) mask) ----------------
-                    const float4 g4 = *reinterpret_cast<const float4 *>(Gw + wave * NRW + 16 * i + 4 * lq);
-                    const float gv[4] = {g4.x, g4.y, g4.z, g4.w};
 #pragma unroll
                     for (int v = 0; v < 4; ++v) {
                         const float *xr = Xb + (tile * 16 + 4 * lq + v) * XS + li;
