@@ -323,7 +323,8 @@ constexpr int TRACE_ALL_FIRST = 16, TRACE_ALL_STEPS = 8;
 // Compute wave w = wr + wu * WR takes row tiles [wr * RTW, (wr + 1) * RTW) and
 // unit tiles {wu + i * WU}. Waves NCW.. are the loaders. Both kinds of wave pass the
 // same workgroup barriers: one before the loop, then per step [one more when
-// WU > 1,] "P partials ready" and "next step ready".
+// WU > 1,] "P partials ready", [when some compute waves own no units, in training
+// mode: "owners done",] and "next step ready".
 template <class S, bool TR>
 __global__ __launch_bounds__(NTHR) void k_train(const TrainArgs a) {
     extern __shared__ __attribute__((aligned(16))) float lds[];
@@ -737,6 +738,11 @@ __global__ __launch_bounds__(NTHR) void k_train(const TrainArgs a) {
                 asm volatile("" ::: "memory");
 
                 // ---- 5. exchange C: all-gather the group's updated slice ---------
+                // the other waves start polling once this workgroup's owners are
+                // done: the group's words are then about to land, and earlier
+                // polls would only load the L2 while exchange B is under way
+                if constexpr (S::NWO < NCW)
+                    if (a.mode == 0) __syncthreads();
                 if (a.mode == 0) {
                     // at most CH word pairs per thread in flight, to bound registers
                     const uint32_t cbase = 8u * (uint32_t)((par * PX + gx) * U * 33);
@@ -903,6 +909,8 @@ __global__ __launch_bounds__(NTHR) void k_train(const TrainArgs a) {
                 if (s + 3 < steps) fetch_idx(q3);
                 q2 = q3;
                 __syncthreads();   // P partials ready
+                if constexpr (S::NWO < NCW)
+                    if (a.mode == 0) __syncthreads();   // owners done
                 __syncthreads();   // next step ready
             }
         }
