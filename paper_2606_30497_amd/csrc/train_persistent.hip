@@ -288,6 +288,23 @@ __device__ __forceinline__ float rsum16(float v) {
     return v;
 }
 __device__ __forceinline__ float sum64(float v) { return xadd32(xadd16(rsum16(v))); }
+// Row sums of four values per lane over each row of 16 lanes, by a transposing
+// butterfly: the lane pairs of rsum16 (li ^ 8, 7 - li within 8, li ^ 2, li ^ 1),
+// but each exchange hands over only the values the partner keeps. Lane li ends
+// with the sum of y[li >> 2] over its row (the same in the four lanes li >> 2
+// share).
+__device__ __forceinline__ float rsum16x4(const float (&y)[4], int li) {
+    const bool b3 = (li & 8) != 0, b2 = (li & 4) != 0;
+    const float k0 = b3 ? y[2] : y[0], k1 = b3 ? y[3] : y[1];   // kept
+    const float g0 = b3 ? y[0] : y[2], g1 = b3 ? y[1] : y[3];   // handed over
+    const float t0 = k0 + dppf<0x128>(g0);                       // row_ror:8
+    const float t1 = k1 + dppf<0x128>(g1);
+    const float kk = b2 ? t1 : t0, gg = b2 ? t0 : t1;
+    float r = kk + dppf<0x141>(gg);                              // row_half_mirror
+    r += dppf<0x4E>(r);                                          // lanes li, li ^ 2
+    r += dppf<0xB1>(r);                                          // lanes li, li ^ 1
+    return r;
+}
 
 // (epoch, step within the epoch) of a step
 struct Pos {
@@ -507,29 +524,20 @@ __global__ __launch_bounds__(NTHR) void k_train(const TrainArgs a) {
                             mbits |= (on ? 1u : 0u) << ((i * NUW + u) * 4 + v);
                             yp[v] = fmaf(on ? z : 0.0f, w2v[u], yp[v]);     // eqs. 12-13
                         }
+                    // lane li of row group g gets the sum of row 4 g + (li >> 2)
+                    const float rowv = rsum16x4(yp, li);
                     if constexpr (DIRECT) {
-                        // every lane of row group g gets the sums of rows 4 g + v;
-                        // lanes with li < 4 store row 4 g + li, so the tile's 16 words
-                        // go out in one store
-                        float rowv = 0.f;
-#pragma unroll
-                        for (int v = 0; v < 4; ++v) {
-                            const float t = rsum16(yp[v]);
-                            rowv = li == v ? t : rowv;
-                        }
-                        // group 0 folds -Y into its partial, so the group sum is the
-                        // residual Ypred - Y and the other groups need no targets
-                        if (li < 4) {
-                            const int row = tile * 16 + 4 * lq + li;
+                        // lanes li = 4 v store row 4 g + v, so the tile's 16 words go
+                        // out in one store; group 0 folds -Y into its partial, so the
+                        // group sum is the residual Ypred - Y and the other groups
+                        // need no targets
+                        if ((li & 3) == 0) {
+                            const int row = tile * 16 + 4 * lq + (li >> 2);
                             const float yv = gx == 0 ? Yb[row] : 0.0f;
                             st1(rA, bA + 8u * (uint32_t)(gx * RMAX + row), pack(rowv - yv, tag), true);
                         }
                     } else {
-#pragma unroll
-                        for (int v = 0; v < 4; ++v) {
-                            const float sv = rsum16(yp[v]);
-                            if (li == 0) Ypart[wu * R + tile * 16 + 4 * lq + v] = sv;
-                        }
+                        if ((li & 3) == 0) Ypart[wu * R + tile * 16 + 4 * lq + (li >> 2)] = rowv;
                     }
                 }
                 if (wave == 0 && lane == 0) s_flags[5] = s + 1;   // the loader may start
