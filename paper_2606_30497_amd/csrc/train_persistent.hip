@@ -83,7 +83,7 @@ struct Shape {
                       PR % SG == 0 && (SG == 1 || SG == 2 || SG == 4), "ownership");
     static constexpr int XS = 36;                          // X tile row stride (floats)
     static constexpr int WS = 36;                          // weight slice row stride
-    static constexpr int PS = U + 1;                       // P partial row stride
+    static constexpr int PS = 36;                          // P partial row stride (per unit, k inner)
     static constexpr int RSW = 32 * U;                     // exchange-B words per workgroup
     static constexpr int GBW = (PR * RSW + PR + 31) / 32 * 32;   // exchange-B words per group
     static constexpr int RPL = R / (8 * NLW);              // rows per loader lane
@@ -91,8 +91,8 @@ struct Shape {
     static constexpr int O_X = 0;                          // [2][R][XS] staged rows
     static constexpr int O_Y = O_X + 2 * R * XS;           // [2][R]
     static constexpr int O_YP = O_Y + 2 * R;               // [WU][R] partial Ypred
-    static constexpr int O_P = O_YP + WU * R;              // [WR][32][PS] P partials
-    static constexpr int O_WSL = O_P + WR * 32 * PS;       // [U][WS] weight slice
+    static constexpr int O_P = O_YP + WU * R;              // [WR][U][PS] P partials
+    static constexpr int O_WSL = O_P + WR * U * PS;        // [U][WS] weight slice
     static constexpr int O_SSE = O_WSL + U * WS;           // [NCW]
     static constexpr int LDS_FLOATS = O_SSE + NCW;
 
@@ -105,7 +105,7 @@ struct Shape {
     static_assert(R <= RMAX && R <= 128, "rows");
     static_assert(PX == 1 || PX == 2 || PX == 4 || PX == 8, "groups");
     static_assert(PR >= 1 && PR <= 32, "workgroups per group");
-    static_assert(O_WSL % 4 == 0, "float4 alignment");
+    static_assert(O_WSL % 4 == 0 && O_P % 4 == 0, "float4 alignment");
 };
 
 // ---------------------------------------------------------------------------
@@ -412,7 +412,7 @@ __global__ __launch_bounds__(NTHR) void k_train(const TrainArgs a) {
     float *Xall = lds + S::O_X;     // [2][R][XS]
     float *Yall = lds + S::O_Y;     // [2][R]
     float *Ypart = lds + S::O_YP;   // [WU][R]
-    float *Pred = lds + S::O_P;     // [WR][32][PS]
+    float *Pred = lds + S::O_P;     // [WR][U][PS]
     float *Wsl = lds + S::O_WSL;    // [U][WS]
     float *SseW = lds + S::O_SSE;   // [NCW]
 
@@ -452,6 +452,7 @@ __global__ __launch_bounds__(NTHR) void k_train(const TrainArgs a) {
                 ow1b = COLD(W1)[(k0 + 1) * H + ug];
                 ow2 = COLD(W2)[ug];
             }
+            const float scale_full = 2.0f / (float)batch, scale_tail = 2.0f / (float)tail;
             // the loss is reduced one step late by wave 1 of workgroup (0, 0)
             const bool lossw = gx == 0 && gb == 0 && wave == 1;
             double epoch_sse = 0.0;
@@ -470,7 +471,7 @@ __global__ __launch_bounds__(NTHR) void k_train(const TrainArgs a) {
                 const int par = s & 1;
                 const int nb = cur.sb == spe - 1 ? tail : batch;
                 const int rc = nb - gb * R;        // rows of this workgroup in the batch (may be <= 0)
-                const float scale = 2.0f / (float)nb;
+                const float scale = cur.sb == spe - 1 ? scale_tail : scale_full;   // 2 / nb
                 const float *Xb = Xall + par * R * XS;
                 const float *Yb = Yall + par * R;
                 const uint32_t bB = 8u * (uint32_t)((par * PX + gx) * S::GBW);   // group block (bytes)
@@ -644,10 +645,10 @@ __global__ __launch_bounds__(NTHR) void k_train(const TrainArgs a) {
                 for (int kt = 0; kt < 2; ++kt)
 #pragma unroll
                     for (int u = 0; u < NUW; ++u) {
+                        // the lane's four k = kt * 16 + 4 lq + v of unit ul, in one store
                         const int ul = (wu + u * WU) * 16 + li;
-#pragma unroll
-                        for (int v = 0; v < 4; ++v)
-                            Pred[(wr * 32 + kt * 16 + 4 * lq + v) * PS + ul] = pacc[kt][u][v];
+                        *reinterpret_cast<float4 *>(Pred + (wr * U + ul) * PS + kt * 16 + 4 * lq) =
+                            make_float4(pacc[kt][u][0], pacc[kt][u][1], pacc[kt][u][2], pacc[kt][u][3]);
                     }
 
                 // deferred loss of the previous step (its words are long written)
@@ -677,8 +678,9 @@ __global__ __launch_bounds__(NTHR) void k_train(const TrainArgs a) {
                     float v0 = 0.f, v1 = 0.f;
 #pragma unroll
                     for (int w = 0; w < WR; ++w) {
-                        v0 += Pred[(w * 32 + k) * PS + ul];
-                        v1 += Pred[(w * 32 + k + 1) * PS + ul];
+                        const float2 pv = *reinterpret_cast<const float2 *>(Pred + (w * U + ul) * PS + k);
+                        v0 += pv.x;
+                        v1 += pv.y;
                     }
                     const int o = ul / UPW, jo = ul - o * UPW;
                     st2(rB, bB + 8u * (uint32_t)((o * PR + gb) * NPAIR + jo * 32 + k), pack(v0, tag),
