@@ -52,7 +52,7 @@ def load_traffic(workload_name):
     return e.get("hbm_bytes_per_launch")
 
 
-def cpu_baseline(w, data, max_seconds=15.0):
+def cpu_baseline(w, data, max_seconds):
     import oracle
     steps = 1
     # size the prefix from a one-step probe so the whole leg takes ~max_seconds
@@ -84,41 +84,14 @@ def copy_calibration(mib):
     print(json.dumps({"copy_calibration_bytes_per_launch": n * 4, "launches": 4}), flush=True)
 
 
-def main():
-    ap = argparse.ArgumentParser()
-    ap.add_argument("--gpus", type=int, default=1)
-    ap.add_argument("--steps", type=int, default=5)
-    ap.add_argument("--warmup", type=int, default=2)
-    ap.add_argument("--workload", type=int, default=4,
-                    help="index into datagen.WORKLOADS (default: the 10M-sample 32-256-1 run)")
-    ap.add_argument("--no-cpu-baseline", action="store_true")
-    ap.add_argument("--copy-calibration", type=int, default=0, metavar="MIB",
-                    help="run only a plain device copy of MIB MiB (4 launches), the reference "
-                         "for scaling the FETCH_SIZE / WRITE_SIZE counters")
-    args = ap.parse_args()
-    if args.copy_calibration:
-        copy_calibration(args.copy_calibration)
-        return
-    if args.gpus != 1:
-        print("bench.py runs on one GPU only: this path is single-GPU by design "
-              "(--gpus %d requested)" % args.gpus, file=sys.stderr)
-        sys.exit(2)
-
-    import numpy as np
-    import torch
-
+def measure(w, args, mlp, torch, np, data=None):
+    """Time args.steps full training runs of workload w; return the JSON record."""
     import datagen
-    from paper_2606_30497_amd import mlp
-
-    if not torch.cuda.is_available():
-        print("bench.py needs a GPU", file=sys.stderr)
-        sys.exit(1)
-    mlp.load(require_built=True)
-    w = datagen.WORKLOADS[args.workload]
-    t0 = time.perf_counter()
-    data = datagen.make_workload(w)
-    print("# data %s generated in %.1f s" % (w.name, time.perf_counter() - t0), file=sys.stderr,
-          flush=True)
+    if data is None:
+        t0 = time.perf_counter()
+        data = datagen.make_workload(w)
+        print("# data %s generated in %.1f s" % (w.name, time.perf_counter() - t0),
+              file=sys.stderr, flush=True)
     dev = torch.device("cuda:0")
     X = torch.from_numpy(data.X).to(dev)
     Y = torch.from_numpy(data.Y).to(dev)
@@ -189,11 +162,53 @@ def main():
         },
         "kernel_launches_per_step": launches,
         "workgroups": wgs,
+        "us_per_sgd_step": float(np.mean(kernel_ms)) * 1e3 / w.steps,
         "final_epoch_loss": final_loss,
     }
     if not args.no_cpu_baseline:
-        out["cpu_baseline"] = cpu_baseline(w, data)
-    print(json.dumps(out), flush=True)
+        out["cpu_baseline"] = cpu_baseline(w, data, args.cpu_seconds)
+    return out
+
+
+def main():
+    ap = argparse.ArgumentParser()
+    ap.add_argument("--gpus", type=int, default=1)
+    ap.add_argument("--steps", type=int, default=5)
+    ap.add_argument("--warmup", type=int, default=2)
+    ap.add_argument("--workload", type=int, default=4,
+                    help="index into datagen.WORKLOADS (default: the 10M-sample 32-256-1 run)")
+    ap.add_argument("--suite", choices=("configs", "sweep", "table1"), default=None,
+                    help="instead of the one headline line, print one line per workload of a "
+                         "suite: the five evaluation workloads, the hidden-width sweep "
+                         "(Table II sizes) or the Table I sizes")
+    ap.add_argument("--no-cpu-baseline", action="store_true")
+    ap.add_argument("--cpu-seconds", type=float, default=15.0,
+                    help="CPU seconds spent on the oracle baseline leg")
+    ap.add_argument("--copy-calibration", type=int, default=0, metavar="MIB",
+                    help="run only a plain device copy of MIB MiB (4 launches), the reference "
+                         "for scaling the FETCH_SIZE / WRITE_SIZE counters")
+    args = ap.parse_args()
+    if args.copy_calibration:
+        copy_calibration(args.copy_calibration)
+        return
+    if args.gpus != 1:
+        print("bench.py runs on one GPU only: this path is single-GPU by design "
+              "(--gpus %d requested)" % args.gpus, file=sys.stderr)
+        sys.exit(2)
+
+    import numpy as np
+    import torch
+
+    import datagen
+    from paper_2606_30497_amd import mlp
+
+    if not torch.cuda.is_available():
+        print("bench.py needs a GPU", file=sys.stderr)
+        sys.exit(1)
+    mlp.load(require_built=True)
+    suite = datagen.SUITES[args.suite] if args.suite else [datagen.WORKLOADS[args.workload]]
+    for w in suite:
+        print(json.dumps(measure(w, args, mlp, torch, np)), flush=True)
 
 
 if __name__ == "__main__":

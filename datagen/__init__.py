@@ -77,6 +77,22 @@ WORKLOADS = [
     Workload("mlp32-256-1_n10M_b4096_e3", 256, 10_000_000, 4096, 0.002, 3, True, 1005),
 ]
 
+# The paper's hidden-width sweep (Sec. VI.C, Table II): n = 2,560 samples,
+# batch 256, lr 0.002 and 100 epochs (the training setup of Sec. III.A), hidden
+# width 32 ... 1024. The paper does not say whether batches are shuffled; these
+# use a seeded per-epoch permutation like the evaluation workloads.
+SWEEP_HIDDEN = (32, 64, 128, 256, 512, 1024)
+SWEEP = [Workload("mlp32-%d-1_n2560_b256_e100" % h, h, 2560, 256, 0.002, 100, True, 2000 + h)
+         for h in SWEEP_HIDDEN]
+
+# The dataset sizes of the paper's strategy comparison (Sec. VI.B, Table I):
+# 256, 2,560 and 25,600 samples of the 32-256-1 net, batch 256, lr 0.002,
+# 100 epochs.
+TABLE1 = [Workload("mlp32-256-1_n%d_b256_e100" % n, 256, n, 256, 0.002, 100, True, 3000 + i)
+          for i, n in enumerate((256, 2560, 25600))]
+
+SUITES = {"configs": WORKLOADS, "sweep": SWEEP, "table1": TABLE1}
+
 
 @dataclasses.dataclass
 class Data:

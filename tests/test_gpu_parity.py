@@ -195,6 +195,20 @@ def test_train_ten_steps_full_workload(mlp, k):
     assert np.all(np.abs(gsl - ref["step_loss"]) <= 1e-3 * np.abs(ref["step_loss"]))
 
 
+@pytest.mark.parametrize("w", datagen.SWEEP, ids=lambda w: w.name)
+def test_sweep_workload_steps(mlp, w):
+    """Hidden-width sweep (Table II sizes): the first 20 steps (two epochs, a fresh
+    permutation each) match the oracle's weights, weight change and step losses."""
+    d = datagen.make_workload(w)
+    g1, g2, gsl, gel = _train_gpu(mlp, d, w.batch, w.lr, w.epochs, max_steps=20, perm=d.perm)
+    ref = oracle.train(d.X, d.Y, d.W1, d.W2, w.batch, w.lr, w.epochs, perm=d.perm, max_steps=20)
+    W10 = d.W1.astype(np.float64)
+    assert rel(g1 - W10, ref["W1"] - W10) <= 1e-3
+    assert rel(g2 - d.W2, ref["W2"] - d.W2.astype(np.float64)) <= 1e-3
+    assert np.all(np.abs(gsl - ref["step_loss"]) <= 1e-3 * np.abs(ref["step_loss"]))
+    assert np.all(np.abs(gel[:2] - ref["epoch_loss"][:2]) <= 1e-3 * ref["epoch_loss"][:2])
+
+
 def test_train_epochs_with_tail_and_shuffle(mlp):
     n, h, B, E, lr = 1000, 256, 64, 3, 0.01
     d = datagen.make_data(n, h, epochs=E, shuffle=True, seed=77)
