@@ -84,6 +84,43 @@ mlp_status mlp_init(mlp_t *out, int32_t d_in, int32_t hidden, int32_t d_out,
 /* Rebind the stream later calls enqueue on. */
 mlp_status mlp_set_stream(mlp_t ctx, void *stream);
 
+/* Training strategies. They change how mlp_backward, mlp_sgd_step and
+ * mlp_train_epochs compute (never what: every strategy computes eqs. 11-19 on
+ * the same rows). MLP_STRATEGY_FUSED is the default; the others exist for the
+ * strategy comparison of the paper's Sec. VI.B (Table I).
+ *   FUSED     all steps of a call in one kernel launch (the persistent
+ *             trainer); batch sizes it has no launch plan for run on TILE
+ *   TILE      per step, one fused kernel (each workgroup a slice of the batch:
+ *             forward, backward and its partial gradients in registers) and
+ *             one fixed-order reduction that applies the update; host loop
+ *   OPTIMIZED the paper's optimized strategy (Sec. V): LDS-tiled products on
+ *             explicitly transposed operands, ReLU fused into the first
+ *             product; one kernel per operation, intermediates in device
+ *             memory, host loop
+ *   BASELINE  the paper's baseline strategy (Sec. IV): one thread per output
+ *             element reading global memory only, separate elementwise
+ *             kernels, intermediates in device memory, host loop */
+typedef enum {
+    MLP_STRATEGY_FUSED = 0,
+    MLP_STRATEGY_TILE = 1,
+    MLP_STRATEGY_OPTIMIZED = 2,
+    MLP_STRATEGY_BASELINE = 3
+} mlp_strategy;
+
+/* Bytes of device memory the strategy needs beyond the context's workspace,
+ * for batches up to max_batch: 0 for FUSED and TILE; for OPTIMIZED and
+ * BASELINE the intermediates of one step (about 4 * max_batch * (6 hidden +
+ * 68) bytes). Returns 0 for an unsupported shape or strategy. */
+size_t mlp_strategy_workspace_bytes(int32_t d_in, int32_t hidden, int64_t max_batch,
+                                    int32_t strategy);
+
+/* Select the strategy of later training calls on ctx. workspace (device,
+ * 256-byte aligned, owned by the caller, kept alive while the strategy is
+ * selected) must hold mlp_strategy_workspace_bytes(32, hidden, max_batch,
+ * strategy) bytes for the context's max_batch; it may be NULL when that is 0.
+ * On error the previous strategy stays selected. */
+mlp_status mlp_set_strategy(mlp_t ctx, int32_t strategy, void *workspace, size_t ws_bytes);
+
 /* Forward pass, eqs. (11)-(13): Ypred[t] = ReLU(X[r_t] W1) W2 for t < B, where
  * r_t = idx[t] (idx == NULL: r_t = t). X has n_rows rows. Ypred is [B].
  * B must be >= 1; it is not limited by max_batch. Weights are not changed. */
@@ -132,9 +169,10 @@ mlp_status mlp_check_errors(mlp_t ctx);
 mlp_status mlp_profile(mlp_t ctx, int32_t enable);
 mlp_status mlp_last_kernel_ms(mlp_t ctx, float *ms);
 
-/* Launch shape of an mlp_train_epochs call with these sizes: the number of
- * workgroups of its training kernel and the total number of kernel launches
- * the call enqueues (launch-count evidence for the benchmark). */
+/* Launch shape of an mlp_train_epochs call with these sizes under the selected
+ * strategy: the number of workgroups of its main training kernel and the total
+ * number of kernel launches the call enqueues (launch-count evidence for the
+ * benchmark). */
 mlp_status mlp_launch_info(mlp_t ctx, int64_t n, int64_t batch, int32_t epochs,
                            int32_t *workgroups, int64_t *launches);
 

@@ -97,6 +97,39 @@ extern "C" mlp_status mlp_init(mlp_t *out, int32_t d_in, int32_t hidden, int32_t
     return MLP_OK;
 }
 
+static bool strategy_valid(int32_t s) {
+    return s == MLP_STRATEGY_FUSED || s == MLP_STRATEGY_TILE || s == MLP_STRATEGY_OPTIMIZED ||
+           s == MLP_STRATEGY_BASELINE;
+}
+
+static bool strategy_hostloop(int32_t s) {
+    return s == MLP_STRATEGY_OPTIMIZED || s == MLP_STRATEGY_BASELINE;
+}
+
+extern "C" size_t mlp_strategy_workspace_bytes(int32_t d_in, int32_t hidden, int64_t max_batch,
+                                               int32_t strategy) {
+    if (d_in != D_IN || !hidden_supported(hidden) || max_batch < 1 || max_batch > MLP_MAX_BATCH ||
+        !strategy_hostloop(strategy))
+        return 0;
+    return round256(sizeof(float) * hostloop_workspace_floats(hidden, max_batch));
+}
+
+extern "C" mlp_status mlp_set_strategy(mlp_t c, int32_t strategy, void *workspace,
+                                       size_t ws_bytes) {
+    if (!c || !strategy_valid(strategy)) return MLP_ERR_INVALID_ARG;
+    if (strategy_hostloop(strategy)) {
+        const size_t need = mlp_strategy_workspace_bytes(D_IN, c->hidden, c->max_batch, strategy);
+        if (!workspace || ws_bytes < need || ((uintptr_t)workspace & 255u)) return MLP_ERR_WORKSPACE;
+        c->hl_ws = (float *)workspace;
+        c->hl_max_batch = c->max_batch;
+    } else {
+        c->hl_ws = nullptr;
+        c->hl_max_batch = 0;
+    }
+    c->strategy = strategy;
+    return MLP_OK;
+}
+
 extern "C" mlp_status mlp_set_stream(mlp_t c, void *stream) {
     if (!c) return MLP_ERR_INVALID_ARG;
     c->stream = (hipStream_t)stream;
@@ -140,13 +173,19 @@ static void prof_end(mlp_ctx *c) {
     c->ev_valid = true;
 }
 
-// The persistent trainer runs every SGD step of a call in one launch; the tile
-// path (two launches per step) serves batches the trainer's plan cannot hold,
-// and every call when MLP_PATH=tile.
+// Under the FUSED strategy the persistent trainer runs every SGD step of a call
+// in one launch; the tile path (two launches per step) serves batches the
+// trainer's plan cannot hold, and every call under the TILE strategy.
 static bool use_persistent(const mlp_ctx *c, int64_t batch, TrainPlan *pl) {
-    const char *path = getenv("MLP_PATH");
-    if (path && strcmp(path, "tile") == 0) return false;
+    if (c->strategy != MLP_STRATEGY_FUSED) return false;
     return plan_train(c->hidden, batch, pl);
+}
+
+// One host-driven step under the TILE, OPTIMIZED or BASELINE strategy.
+static hipError_t host_step(const mlp_ctx *c, const float *X, int64_t n_rows, const float *Y,
+                            const int32_t *idx, int64_t idx_off, int64_t nb, const ReduceArgs &a) {
+    if (strategy_hostloop(c->strategy)) return hostloop_step(*c, X, n_rows, Y, idx, idx_off, nb, a);
+    return tile_step(*c, X, n_rows, Y, idx, idx_off, nb, a);
 }
 
 static TrainArgs train_args(const mlp_ctx *c, const TrainPlan &pl) {
@@ -180,7 +219,7 @@ extern "C" mlp_status mlp_backward(mlp_t c, const float *X, int64_t n_rows, cons
     a.dW1 = dW1;
     a.dW2 = dW2;
     a.loss = loss;
-    return hip_status(tile_step(*c, X, n_rows, Y, idx, 0, B, a));
+    return hip_status(host_step(c, X, n_rows, Y, idx, 0, B, a));
 }
 
 extern "C" mlp_status mlp_sgd_step(mlp_t c, const float *X, int64_t n_rows, const float *Y,
@@ -203,7 +242,7 @@ extern "C" mlp_status mlp_sgd_step(mlp_t c, const float *X, int64_t n_rows, cons
         a.sgd = 1;
         a.lr = lr;
         a.loss = loss;
-        st = hip_status(tile_step(*c, X, n_rows, Y, idx, 0, B, a));
+        st = hip_status(host_step(c, X, n_rows, Y, idx, 0, B, a));
     }
     prof_end(c);
     return st;
@@ -254,7 +293,7 @@ extern "C" mlp_status mlp_train_epochs(mlp_t c, const float *X, const float *Y, 
             a.epoch = ep;
             a.first_in_epoch = s == 0;
             const int32_t *ix = perm ? perm + (int64_t)ep * n : nullptr;
-            e = tile_step(*c, X, n, Y, ix, off, nb, a);
+            e = host_step(c, X, n, Y, ix, off, nb, a);
             if (e != hipSuccess) break;
             ++step;
         }
@@ -301,8 +340,15 @@ extern "C" mlp_status mlp_launch_info(mlp_t c, int64_t n, int64_t batch, int32_t
         *launches = 1;
         return MLP_OK;
     }
+    const int64_t steps = ((n + batch - 1) / batch) * (int64_t)epochs;
+    if (strategy_hostloop(c->strategy)) {
+        // the largest product grid: 16 x 16 blocks over [batch x hidden]
+        *workgroups = (int32_t)(((batch + 15) / 16) * ((c->hidden + 15) / 16));
+        *launches = hostloop_launches_per_step(c->strategy) * steps + 1;
+        return MLP_OK;
+    }
     const int R = tile_rows_per_wg(batch);
     *workgroups = (int32_t)((batch + R - 1) / R);
-    *launches = 2 * ((n + batch - 1) / batch) * (int64_t)epochs + (epochs > 0 ? 1 : 0);
+    *launches = 2 * steps + 1;
     return MLP_OK;
 }

@@ -94,6 +94,9 @@ struct Ctx {
     int device = 0;
     int num_cu = 0;
     bool profile = false;
+    int strategy = MLP_STRATEGY_FUSED;
+    float *hl_ws = nullptr;       // OPTIMIZED / BASELINE intermediates (caller's memory)
+    int64_t hl_max_batch = 0;     // batch the strategy workspace was sized for
     hipEvent_t ev0 = nullptr, ev1 = nullptr;
     bool ev_valid = false;
 };
@@ -124,6 +127,12 @@ hipError_t tile_step(const Ctx &c, const float *X, int64_t n_rows, const float *
                      const int32_t *idx, int64_t idx_off, int64_t nb, const ReduceArgs &a);
 hipError_t clear_control(const Ctx &c);
 hipError_t clear_words(const Ctx &c, uint64_t *p, int64_t n);
+
+// Host-loop strategies of the paper (hostloop.hip)
+size_t hostloop_workspace_floats(int hidden, int64_t max_batch);
+int hostloop_launches_per_step(int strategy);
+hipError_t hostloop_step(const Ctx &c, const float *X, int64_t n_rows, const float *Y,
+                         const int32_t *idx, int64_t idx_off, int64_t nb, const ReduceArgs &a);
 
 // Persistent trainer
 bool plan_train(int hidden, int64_t batch, TrainPlan *plan);

@@ -23,7 +23,12 @@ MLP_OK = 0
 STATUS = {0: "MLP_OK", -1: "MLP_ERR_INVALID_ARG", -2: "MLP_ERR_UNSUPPORTED",
           -3: "MLP_ERR_WORKSPACE", -4: "MLP_ERR_HIP", -6: "MLP_ERR_INDEX"}
 
-EXPORTS = ("mlp_workspace_bytes", "mlp_init", "mlp_set_stream", "mlp_forward", "mlp_backward",
+STRATEGY_FUSED, STRATEGY_TILE, STRATEGY_OPTIMIZED, STRATEGY_BASELINE = 0, 1, 2, 3
+STRATEGIES = {"fused": STRATEGY_FUSED, "tile": STRATEGY_TILE, "optimized": STRATEGY_OPTIMIZED,
+              "baseline": STRATEGY_BASELINE}
+
+EXPORTS = ("mlp_workspace_bytes", "mlp_init", "mlp_set_stream", "mlp_strategy_workspace_bytes",
+           "mlp_set_strategy", "mlp_forward", "mlp_backward",
            "mlp_sgd_step", "mlp_train_epochs", "mlp_check_errors", "mlp_profile",
            "mlp_last_kernel_ms", "mlp_launch_info", "mlp_destroy", "mlp_status_string")
 
@@ -62,6 +67,8 @@ def load(require_built: bool = True):
         "mlp_init": (ctypes.c_int, [ctypes.POINTER(_vp), _i32, _i32, _i32, _i64, _vp, _vp, _vp,
                                     ctypes.c_size_t, _vp]),
         "mlp_set_stream": (ctypes.c_int, [_vp, _vp]),
+        "mlp_strategy_workspace_bytes": (ctypes.c_size_t, [_i32, _i32, _i64, _i32]),
+        "mlp_set_strategy": (ctypes.c_int, [_vp, _i32, _vp, ctypes.c_size_t]),
         "mlp_forward": (ctypes.c_int, [_vp, _vp, _i64, _vp, _i64, _vp]),
         "mlp_backward": (ctypes.c_int, [_vp, _vp, _i64, _vp, _vp, _i64, _vp, _vp, _vp]),
         "mlp_sgd_step": (ctypes.c_int, [_vp, _vp, _i64, _vp, _vp, _i64, _f32, _vp]),
@@ -114,6 +121,7 @@ class Context:
         self.W1, self.W2, self.workspace = W1, W2, workspace
         self.max_batch = max_batch
         self.hidden = W1.shape[1]
+        self.strategy_workspace = None
 
     def __del__(self):
         h, self.handle = getattr(self, "handle", None), None
@@ -147,6 +155,23 @@ def mlp_init(W1: torch.Tensor, W2: torch.Tensor, max_batch: int, workspace=None,
 
 def mlp_set_stream(ctx: Context, stream) -> None:
     _check("mlp_set_stream", load().mlp_set_stream(ctx.handle, stream))
+
+
+def mlp_strategy_workspace_bytes(d_in: int, hidden: int, max_batch: int, strategy: int) -> int:
+    return int(load().mlp_strategy_workspace_bytes(d_in, hidden, max_batch, strategy))
+
+
+def mlp_set_strategy(ctx: Context, strategy, workspace=None) -> None:
+    """Select the training strategy (a name of STRATEGIES or its code); allocates
+    the strategy workspace as a torch tensor when none is given."""
+    code = STRATEGIES[strategy] if isinstance(strategy, str) else int(strategy)
+    need = mlp_strategy_workspace_bytes(D_IN, ctx.hidden, ctx.max_batch, code)
+    if workspace is None and need > 0:
+        workspace = torch.empty(need, dtype=torch.uint8, device=ctx.W1.device)
+    ptr = _dev(workspace, "workspace", dtype=torch.uint8, numel=need) if workspace is not None else None
+    nbytes = workspace.numel() if workspace is not None else 0
+    _check("mlp_set_strategy", load().mlp_set_strategy(ctx.handle, code, ptr, nbytes))
+    ctx.strategy_workspace = workspace
 
 
 def _rows(idx, B, name="idx"):

@@ -50,6 +50,20 @@ def test_workspace_bytes():
     assert lib.mlp_workspace_bytes(32, 256, (1 << 20) + 1) == 0
 
 
+def test_strategy_workspace_bytes():
+    lib = _lib()
+    for h in (32, 256, 1024):
+        for strat in (2, 3):   # OPTIMIZED, BASELINE: intermediates of one step
+            b = lib.mlp_strategy_workspace_bytes(32, h, 256, strat)
+            assert b % 256 == 0 and b >= 4 * 256 * (6 * h + 68)
+            assert lib.mlp_strategy_workspace_bytes(32, h, 4096, strat) > b
+        for strat in (0, 1):   # FUSED, TILE need none
+            assert lib.mlp_strategy_workspace_bytes(32, h, 256, strat) == 0
+    assert lib.mlp_strategy_workspace_bytes(32, 256, 256, 4) == 0
+    assert lib.mlp_strategy_workspace_bytes(32, 100, 256, 2) == 0
+    assert lib.mlp_strategy_workspace_bytes(32, 256, 0, 2) == 0
+
+
 def test_status_strings():
     lib = _lib()
     for s in (0, -1, -2, -3, -4, -6):
@@ -87,4 +101,5 @@ def test_null_context_is_rejected():
     assert lib.mlp_train_epochs(None, fake, fake, 10, 2, 0.1, 1, None, -1, None, None) == -1
     assert lib.mlp_check_errors(None) == -1
     assert lib.mlp_profile(None, 1) == -1
+    assert lib.mlp_set_strategy(None, 0, None, 0) == -1
     lib.mlp_destroy(None)

@@ -40,10 +40,13 @@ def _to(a, dtype=None):
     return t.cuda()
 
 
-def _ctx(mlp, W1, W2, max_batch):
+def _ctx(mlp, W1, W2, max_batch, strategy=None):
     w1 = _to(W1.astype(np.float32))
     w2 = _to(np.reshape(W2, -1).astype(np.float32))
-    return mlp.mlp_init(w1, w2, max_batch), w1, w2
+    ctx = mlp.mlp_init(w1, w2, max_batch)
+    if strategy is not None:
+        mlp.mlp_set_strategy(ctx, strategy)
+    return ctx, w1, w2
 
 
 def _rows(rng, n, B):
@@ -69,10 +72,10 @@ def test_forward_matches_oracle(mlp, h):
 
 # --- per-step gradients ----------------------------------------------------------
 
-def _check_grad(mlp, h, B, n=5000, seed=0, idx_none=False):
+def _check_grad(mlp, h, B, n=5000, seed=0, idx_none=False, strategy=None):
     rng = np.random.default_rng(seed)
     d = datagen.make_data(n, h, seed=200 + h + B, with_perm=False)
-    ctx, _, _ = _ctx(mlp, d.W1, d.W2, max(B, 1))
+    ctx, _, _ = _ctx(mlp, d.W1, d.W2, max(B, 1), strategy)
     idx = None if idx_none else _rows(rng, n, B)
     dW1, dW2, loss = mlp.mlp_backward(ctx, _to(d.X), _to(d.Y), None if idx is None else _to(idx),
                                       B=B)
@@ -162,8 +165,8 @@ def _workload_data(k):
     return _DATA[k]
 
 
-def _train_gpu(mlp, d, batch, lr, epochs, max_steps=-1, perm=None):
-    ctx, w1, w2 = _ctx(mlp, d.W1, d.W2, batch)
+def _train_gpu(mlp, d, batch, lr, epochs, max_steps=-1, perm=None, strategy=None):
+    ctx, w1, w2 = _ctx(mlp, d.W1, d.W2, batch, strategy)
     n = d.X.shape[0]
     spe = -(-n // batch)
     steps = spe * epochs if max_steps < 0 else min(max_steps, spe * epochs)
@@ -373,16 +376,73 @@ def test_coherent_fallback_is_bitwise_identical(mlp):
             assert np.array_equal(x, y)
 
 
+@pytest.mark.parametrize("strategy", ["tile", "optimized", "baseline"])
 @pytest.mark.parametrize("h,B", [(256, 256), (1024, 1024), (32, 100)])
-def test_tile_path_matches_oracle(mlp, h, B):
-    with _env(MLP_PATH="tile"):
-        _check_grad(mlp, h, B, n=5000, seed=3)
-        n, E, lr = 1500, 2, 0.01
-        d = datagen.make_data(n, h, epochs=E, shuffle=True, seed=93 + h)
-        g1, g2, gsl, gel = _train_gpu(mlp, d, B, lr, E, perm=d.perm)
+def test_host_loop_strategy_matches_oracle(mlp, strategy, h, B):
+    _check_grad(mlp, h, B, n=5000, seed=3, strategy=strategy)
+    n, E, lr = 1500, 2, 0.01
+    d = datagen.make_data(n, h, epochs=E, shuffle=True, seed=93 + h)
+    g1, g2, gsl, gel = _train_gpu(mlp, d, B, lr, E, perm=d.perm, strategy=strategy)
     ref = oracle.train(d.X, d.Y, d.W1, d.W2, B, lr, E, perm=d.perm)
     assert rel(g1 - d.W1, ref["W1"] - d.W1.astype(np.float64)) <= 1e-3
+    assert rel(g2 - d.W2, ref["W2"] - d.W2.astype(np.float64)) <= 1e-3
+    assert np.all(np.abs(gsl - ref["step_loss"]) <= 1e-3 * ref["step_loss"])
     assert np.all(np.abs(gel - ref["epoch_loss"]) <= 1e-3 * ref["epoch_loss"])
+
+
+@pytest.mark.parametrize("strategy", ["optimized", "baseline"])
+@pytest.mark.parametrize("B", [1, 7, 64, 160, 1000])
+def test_paper_strategy_small_batches(mlp, strategy, B):
+    for h in (32, 256, 1024):
+        _check_grad(mlp, h, B, seed=B, strategy=strategy)
+
+
+@pytest.mark.parametrize("strategy", ["optimized", "baseline"])
+def test_paper_strategy_worked_step_exact(mlp, strategy):
+    import json, os
+    g = json.load(open(os.path.join(os.path.dirname(__file__), "golden", "worked_two_sample.json")))
+    X, W1, W2 = _embed(np.array(g["X"], np.float32), np.array(g["W1"]), np.array(g["W2"]), 256)
+    Y = np.array(g["Y"], np.float32)
+    ctx, w1, w2 = _ctx(mlp, W1, W2, 2, strategy)
+    dW1, dW2, loss = mlp.mlp_backward(ctx, _to(X), _to(Y))
+    exp1 = np.zeros((32, 256)); exp1[:2, :2] = g["dW1"]
+    exp2 = np.zeros(256); exp2[:2] = g["dW2"]
+    assert np.array_equal(dW1.cpu().numpy(), exp1) and np.array_equal(dW2.cpu().numpy(), exp2)
+    assert float(loss.cpu()[0]) == g["loss"]
+
+
+def test_paper_strategies_agree_bitwise(mlp):
+    """The two strategies of the paper form every output with the same products
+    in the same k order (only where operands live differs), so a training run
+    gives bitwise equal weights and losses under both."""
+    n, h, B, E, lr = 2560, 256, 256, 2, 0.002
+    d = datagen.make_data(n, h, epochs=E, shuffle=True, seed=94)
+    a = _train_gpu(mlp, d, B, lr, E, perm=d.perm, strategy="optimized")
+    b = _train_gpu(mlp, d, B, lr, E, perm=d.perm, strategy="baseline")
+    for x, y in zip(a, b):
+        assert np.array_equal(x, y)
+
+
+def test_strategy_workspace_checks(mlp):
+    d = datagen.make_data(64, 256, seed=4, with_perm=False)
+    ctx, _, _ = _ctx(mlp, d.W1, d.W2, 256)
+    need = mlp.mlp_strategy_workspace_bytes(32, 256, 256, mlp.STRATEGY_OPTIMIZED)
+    assert need > 0 and need % 256 == 0
+    assert mlp.mlp_strategy_workspace_bytes(32, 256, 256, mlp.STRATEGY_FUSED) == 0
+    small = torch.empty(need - 256, dtype=torch.uint8, device="cuda")
+    with pytest.raises(ValueError):              # the binding's own size check
+        mlp.mlp_set_strategy(ctx, "optimized", small)
+    lib = mlp.load()                             # the library's check, past the binding
+    assert lib.mlp_set_strategy(ctx.handle, mlp.STRATEGY_OPTIMIZED, small.data_ptr(),
+                                small.numel()) == -3
+    assert lib.mlp_set_strategy(ctx.handle, mlp.STRATEGY_OPTIMIZED, None, 0) == -3
+    with pytest.raises(mlp.MLPError):
+        mlp.mlp_set_strategy(ctx, 7)
+    wg, launches = mlp.mlp_launch_info(ctx, 2560, 256, 100)
+    assert launches == 1                        # still the fused strategy
+    mlp.mlp_set_strategy(ctx, "baseline")
+    wg, launches = mlp.mlp_launch_info(ctx, 2560, 256, 100)
+    assert launches == 11 * 10 * 100 + 1
 
 
 def test_launch_info_single_launch(mlp):
@@ -390,8 +450,8 @@ def test_launch_info_single_launch(mlp):
     ctx, _, _ = _ctx(mlp, d.W1, d.W2, 4096)
     wg, launches = mlp.mlp_launch_info(ctx, 10_000_000, 4096, 3)
     assert launches == 1 and wg == 256
-    with _env(MLP_PATH="tile"):
-        wg, launches = mlp.mlp_launch_info(ctx, 10_000, 4096, 3)
+    mlp.mlp_set_strategy(ctx, "tile")
+    wg, launches = mlp.mlp_launch_info(ctx, 10_000, 4096, 3)
     assert launches == 2 * 3 * 3 + 1
 
 
