@@ -175,6 +175,55 @@ def measure(w, args, mlp, torch, np, data=None):
     return out
 
 
+def measure_forward(h, X, args, mlp, torch, np):
+    """mlp_forward over every row of X (resident in HBM) with a 32-h-1 net: rows/s
+    and the fraction of the fp32 MFMA peak (66 h FLOP per row: 2*32*h of eq. 11 on
+    the matrix cores plus 2*h of eq. 13) and of HBM bandwidth (132 B per row)."""
+    import datagen
+    d = datagen.make_data(1, h, seed=2000 + h, with_perm=False)
+    dev = X.device
+    W1 = torch.from_numpy(d.W1).to(dev)
+    W2 = torch.from_numpy(d.W2).to(dev)
+    ctx = mlp.mlp_init(W1, W2, 64)
+    n = X.shape[0]
+    out = torch.empty(n, dtype=torch.float32, device=dev)
+    for _ in range(args.warmup):
+        mlp.mlp_forward(ctx, X, out=out)
+    torch.cuda.synchronize()
+    mlp.mlp_check_errors(ctx)
+    ev = [(torch.cuda.Event(enable_timing=True), torch.cuda.Event(enable_timing=True))
+          for _ in range(args.steps)]
+    t0 = time.perf_counter()
+    for e0, e1 in ev:
+        e0.record()
+        mlp.mlp_forward(ctx, X, out=out)
+        e1.record()
+    torch.cuda.synchronize()
+    t1 = time.perf_counter()
+    mlp.mlp_check_errors(ctx)
+    ms = float(np.mean([e0.elapsed_time(e1) for e0, e1 in ev]))
+    flop = 66.0 * h * n
+    achieved = flop / (ms / 1e3) / 1e12
+    return {
+        "metric": "forward rows/sec (eqs. 11-13 over a resident dataset)",
+        "value": n / ((t1 - t0) / args.steps),
+        "unit": "rows/s",
+        "n_gpus": 1,
+        "steps": args.steps,
+        "warmup": args.warmup,
+        "ms_per_step": (t1 - t0) / args.steps * 1e3,
+        "higher_is_better": True,
+        "dtype": "f32",
+        "data": "synthetic",
+        "config": {"workload": "forward_mlp32-%d-1_n%d" % (h, n), "hidden": h, "n": n},
+        "roofline": {"bound": "mfma", "achieved": achieved, "peak": FP32_PEAK_TFLOPS,
+                     "unit": "TFLOP/s", "frac": achieved / FP32_PEAK_TFLOPS,
+                     "kernel_ms": ms, "flop_per_launch": flop,
+                     "hbm_gbs": 132.0 * n / (ms / 1e3) / 1e9,
+                     "hbm_frac": 132.0 * n / (ms / 1e3) / 1e9 / HBM_PEAK_GBS},
+    }
+
+
 def main():
     ap = argparse.ArgumentParser()
     ap.add_argument("--gpus", type=int, default=1)
@@ -182,10 +231,11 @@ def main():
     ap.add_argument("--warmup", type=int, default=2)
     ap.add_argument("--workload", type=int, default=4,
                     help="index into datagen.WORKLOADS (default: the 10M-sample 32-256-1 run)")
-    ap.add_argument("--suite", choices=("configs", "sweep", "table1"), default=None,
+    ap.add_argument("--suite", choices=("configs", "sweep", "table1", "forward"), default=None,
                     help="instead of the one headline line, print one line per workload of a "
                          "suite: the five evaluation workloads, the hidden-width sweep "
-                         "(Table II sizes) or the Table I sizes")
+                         "(Table II sizes), the Table I sizes, or mlp_forward over the "
+                         "10M-row dataset at every hidden width")
     ap.add_argument("--strategy", choices=("fused", "tile", "optimized", "baseline"),
                     default="fused",
                     help="training strategy (the paper's baseline and optimized strategies, "
@@ -215,6 +265,13 @@ def main():
         print("bench.py needs a GPU", file=sys.stderr)
         sys.exit(1)
     mlp.load(require_built=True)
+    if args.suite == "forward":
+        w = datagen.WORKLOADS[4]
+        data = datagen.make_data(w.n, 32, seed=w.seed, with_perm=False)
+        X = torch.from_numpy(data.X).to("cuda:0")
+        for h in datagen.SWEEP_HIDDEN:
+            print(json.dumps(measure_forward(h, X, args, mlp, torch, np)), flush=True)
+        return
     suite = datagen.SUITES[args.suite] if args.suite else [datagen.WORKLOADS[args.workload]]
     for w in suite:
         print(json.dumps(measure(w, args, mlp, torch, np)), flush=True)

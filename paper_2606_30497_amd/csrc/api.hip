@@ -147,7 +147,7 @@ extern "C" mlp_status mlp_forward(mlp_t c, const float *X, int64_t n_rows, const
                                   int64_t B, float *Ypred) {
     if (!c || !X || !Ypred || B < 1 || n_rows < 1) return MLP_ERR_INVALID_ARG;
     if (!idx && B > n_rows) return MLP_ERR_INVALID_ARG;
-    return hip_status(tile_forward(*c, X, n_rows, idx, B, Ypred));
+    return hip_status(launch_forward(*c, X, n_rows, idx, B, Ypred));
 }
 
 static ReduceArgs base_args(const mlp_ctx *c, int64_t nb) {

@@ -3,16 +3,17 @@
 // Sec. III (eqs. 11-19), d = 32, no biases.
 //
 // Kernels in this file (the "tile" path):
-//   k_tile<H, FWD>  one workgroup owns a contiguous slice of the batch; thread j
+//   k_tile<H>       one workgroup owns a contiguous slice of the batch; thread j
 //                   owns hidden unit j. Rows are staged through LDS in groups of
 //                   RG; Z1, the ReLU mask, H and dZ1 live only in registers
-//                   (never in HBM). With FWD the kernel writes Ypred (eq. 13);
-//                   otherwise it writes the workgroup's partial dW1 = X^T dZ1,
-//                   dW2 = H^T dZ2 and sum of squared residuals to its slot.
+//                   (never in HBM). It writes the workgroup's partial
+//                   dW1 = X^T dZ1, dW2 = H^T dZ2 and sum of squared residuals
+//                   to its slot.
 //   k_reduce<H>     sums the slots in slot order (deterministic), then either
 //                   writes dW1/dW2/loss or applies W -= lr dW (eq. 19) and
 //                   records the step and epoch loss.
-// The persistent single-launch trainer lives in train_persistent.hip.
+// The persistent single-launch trainer lives in train_persistent.hip, the
+// forward pass of mlp_forward in forward.hip.
 #include <hip/hip_runtime.h>
 
 #include <math.h>
@@ -55,12 +56,12 @@ __device__ __forceinline__ int64_t fetch_row(const int32_t *__restrict__ idx, in
     return r;
 }
 
-template <int H, bool FWD>
+template <int H>
 __global__ __launch_bounds__(TileShape<H>::NT) void k_tile(
     const float *__restrict__ X, int64_t n_rows, const float *__restrict__ Y,
     const int32_t *__restrict__ idx, int64_t idx_off, int64_t nb, int rows_per_wg,
     const float *__restrict__ W1, const float *__restrict__ W2, float *__restrict__ partial,
-    int64_t slot_stride, float *__restrict__ ypred_out, int32_t *err) {
+    int64_t slot_stride, int32_t *err) {
     constexpr int NT = TileShape<H>::NT;
     constexpr int NW = TileShape<H>::NW;
     __shared__ float xs[RG][D_IN];
@@ -95,7 +96,7 @@ __global__ __launch_bounds__(TileShape<H>::NT) void k_tile(
         if (j < RG) {
             const int64_t t = tg + j;
             float v = 0.0f;
-            if (!FWD && t < t1) v = Y[fetch_row(idx, idx_off, t, n_rows, err)];
+            if (t < t1) v = Y[fetch_row(idx, idx_off, t, n_rows, err)];
             ys[j] = v;
         }
         __syncthreads();
@@ -118,32 +119,26 @@ __global__ __launch_bounds__(TileShape<H>::NT) void k_tile(
             yp[j] = s;
         }
         __syncthreads();
-        if (FWD) {
-            if (j < RG && tg + j < t1) ypred_out[tg + j] = yp[j];
-        } else {
 #pragma unroll
-            for (int rr = 0; rr < RG; ++rr) {
-                const float res = yp[rr] - ys[rr];
-                const float g = scale * res;                                    // eq. 15
-                if (j == 0) sse = fmaf(res, res, sse);                          // eq. 14
-                const bool on = z[rr] > 0.0f;                                   // ReLU'(z) = [z > 0]
-                q = fmaf(on ? z[rr] : 0.0f, g, q);                              // eq. 16
-                const float dz = on ? g * w2 : 0.0f;                            // eq. 17
+        for (int rr = 0; rr < RG; ++rr) {
+            const float res = yp[rr] - ys[rr];
+            const float g = scale * res;                                        // eq. 15
+            if (j == 0) sse = fmaf(res, res, sse);                              // eq. 14
+            const bool on = z[rr] > 0.0f;                                       // ReLU'(z) = [z > 0]
+            q = fmaf(on ? z[rr] : 0.0f, g, q);                                  // eq. 16
+            const float dz = on ? g * w2 : 0.0f;                                // eq. 17
 #pragma unroll
-                for (int k = 0; k < D_IN; ++k) p[k] = fmaf(xs[rr][k], dz, p[k]); // eq. 18
-            }
+            for (int k = 0; k < D_IN; ++k) p[k] = fmaf(xs[rr][k], dz, p[k]);     // eq. 18
         }
         __syncthreads();
     }
-    if (!FWD) {
-        float *slot = partial + (int64_t)blockIdx.x * slot_stride;
-        if (unit) {
+    float *slot = partial + (int64_t)blockIdx.x * slot_stride;
+    if (unit) {
 #pragma unroll
-            for (int k = 0; k < D_IN; ++k) slot[k * H + j] = p[k];
-            slot[D_IN * H + j] = q;
-        }
-        if (j == 0) slot[(D_IN + 1) * H] = sse;
+        for (int k = 0; k < D_IN; ++k) slot[k * H + j] = p[k];
+        slot[D_IN * H + j] = q;
     }
+    if (j == 0) slot[(D_IN + 1) * H] = sse;
 }
 
 // Fixed-order reduction of G slots. Thread t owns output t of the flattened
@@ -196,19 +191,12 @@ __global__ void k_clear_ctl(Control *c) {
 // ---------------------------------------------------------------------------
 
 template <int H>
-static hipError_t launch_tile(const Ctx &c, bool fwd, const float *X, int64_t n_rows,
-                              const float *Y, const int32_t *idx, int64_t idx_off, int64_t nb,
-                              int rows_per_wg, int G, float *ypred) {
+static hipError_t launch_tile(const Ctx &c, const float *X, int64_t n_rows, const float *Y,
+                              const int32_t *idx, int64_t idx_off, int64_t nb, int rows_per_wg,
+                              int G) {
     constexpr int NT = TileShape<H>::NT;
-    int32_t *err = &c.ctl->err;
-    if (fwd)
-        hipLaunchKernelGGL((k_tile<H, true>), dim3(G), dim3(NT), 0, c.stream, X, n_rows, Y, idx,
-                           idx_off, nb, rows_per_wg, c.W1, c.W2, c.slots, c.slot_stride, ypred,
-                           err);
-    else
-        hipLaunchKernelGGL((k_tile<H, false>), dim3(G), dim3(NT), 0, c.stream, X, n_rows, Y, idx,
-                           idx_off, nb, rows_per_wg, c.W1, c.W2, c.slots, c.slot_stride, ypred,
-                           err);
+    hipLaunchKernelGGL((k_tile<H>), dim3(G), dim3(NT), 0, c.stream, X, n_rows, Y, idx, idx_off, nb,
+                       rows_per_wg, c.W1, c.W2, c.slots, c.slot_stride, &c.ctl->err);
     return hipGetLastError();
 }
 
@@ -231,15 +219,6 @@ static hipError_t launch_reduce(const Ctx &c, int G, const ReduceArgs &a) {
     default: return hipErrorInvalidValue;       \
     }
 
-hipError_t tile_forward(const Ctx &c, const float *X, int64_t n_rows, const int32_t *idx,
-                        int64_t B, float *ypred) {
-    const int R = 64;
-    const int64_t G = (B + R - 1) / R;
-    if (G > 0x7fffffff) return hipErrorInvalidValue;
-    MLP_DISPATCH_H(c.hidden, return launch_tile<HH>(c, true, X, n_rows, nullptr, idx, 0, B, R,
-                                                    (int)G, ypred));
-}
-
 // Rows per workgroup for a batch of nb rows: at most TILE_SLOTS workgroups.
 int tile_rows_per_wg(int64_t nb) {
     int64_t r = (nb + TILE_SLOTS - 1) / TILE_SLOTS;
@@ -253,7 +232,7 @@ hipError_t tile_step(const Ctx &c, const float *X, int64_t n_rows, const float *
     const int G = (int)((nb + R - 1) / R);
     hipError_t e;
     MLP_DISPATCH_H(c.hidden, {
-        e = launch_tile<HH>(c, false, X, n_rows, Y, idx, idx_off, nb, R, G, nullptr);
+        e = launch_tile<HH>(c, X, n_rows, Y, idx, idx_off, nb, R, G);
         if (e != hipSuccess) return e;
         return launch_reduce<HH>(c, G, a);
     });

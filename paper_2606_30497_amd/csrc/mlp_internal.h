@@ -121,8 +121,8 @@ struct ReduceArgs {
 size_t slot_stride_floats(int hidden);
 int tile_rows_per_wg(int64_t nb);
 
-hipError_t tile_forward(const Ctx &c, const float *X, int64_t n_rows, const int32_t *idx,
-                        int64_t B, float *ypred);
+hipError_t launch_forward(const Ctx &c, const float *X, int64_t n_rows, const int32_t *idx,
+                          int64_t B, float *ypred);
 hipError_t tile_step(const Ctx &c, const float *X, int64_t n_rows, const float *Y,
                      const int32_t *idx, int64_t idx_off, int64_t nb, const ReduceArgs &a);
 hipError_t clear_control(const Ctx &c);

@@ -70,6 +70,40 @@ def test_forward_matches_oracle(mlp, h):
     mlp.mlp_check_errors(ctx)
 
 
+@pytest.mark.parametrize("h", H_ALL)
+@pytest.mark.parametrize("B", [1, 15, 16, 17, 1000])
+def test_forward_ragged_batches(mlp, h, B):
+    d = datagen.make_data(1200, h, seed=110 + h, with_perm=False)
+    ctx, _, _ = _ctx(mlp, d.W1, d.W2, 64)
+    idx = np.random.default_rng(B).integers(0, 1200, size=B).astype(np.int32)
+    out = torch.full((B + 40,), 7.0, device="cuda")        # guard words past B stay untouched
+    mlp.mlp_forward(ctx, _to(d.X), _to(idx), B=B, out=out)
+    got = out.cpu().numpy()
+    assert rel(got[:B], oracle.forward(d.X, d.W1, d.W2, idx=idx)) < 1e-5
+    assert np.all(got[B:] == 7.0)
+    mlp.mlp_check_errors(ctx)
+
+
+@pytest.mark.parametrize("k", [3, 4])
+def test_forward_full_dataset_sampled(mlp, k):
+    """mlp_forward over every row of the 1M-row (h = 1024) and 10M-row (h = 256)
+    datasets, in the launch shape of the forward benchmark; 20,000 sampled outputs
+    against the oracle, and every output finite."""
+    w, d = _workload_data(k)
+    print("workload", w.name, flush=True)
+    ctx, _, _ = _ctx(mlp, d.W1, d.W2, 64)
+    X = _to(d.X)
+    out = mlp.mlp_forward(ctx, X)
+    torch.cuda.synchronize()
+    mlp.mlp_check_errors(ctx)
+    assert bool(torch.isfinite(out).all())
+    sample = np.random.default_rng(k).integers(0, w.n, size=20000).astype(np.int64)
+    sample[:2] = [0, w.n - 1]
+    got = out.cpu().numpy()[sample]
+    ref = oracle.forward(d.X, d.W1, d.W2, idx=sample.astype(np.int32))
+    assert rel(got, ref) < 1e-5
+
+
 # --- per-step gradients ----------------------------------------------------------
 
 def _check_grad(mlp, h, B, n=5000, seed=0, idx_none=False, strategy=None):
