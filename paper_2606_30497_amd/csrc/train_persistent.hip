@@ -403,7 +403,8 @@ __global__ __launch_bounds__(NTHR) void k_train(const TrainArgs a) {
                 ow1b = COLD(W1)[(k0 + 1) * H + ug];
                 ow2 = COLD(W2)[ug];
             }
-            const float scale_full = 2.0f / (float)batch, scale_tail = 2.0f / (float)tail;
+            float scale_full = 2.0f / (float)batch, scale_tail = 2.0f / (float)tail;
+            asm volatile("" : "+v"(scale_full), "+v"(scale_tail));   // computed once, selected per step
             // the loss is reduced one step late by wave 1 of workgroup (0, 0)
             const bool lossw = gx == 0 && gb == 0 && wave == 1;
             double epoch_sse = 0.0;
@@ -458,6 +459,9 @@ __global__ __launch_bounds__(NTHR) void k_train(const TrainArgs a) {
                     const float4 xa = *reinterpret_cast<const float4 *>(xr);
                     const float4 xb = *reinterpret_cast<const float4 *>(xr + 4);
                     const float xv[8] = {xa.x, xa.y, xa.z, xa.w, xb.x, xb.y, xb.z, xb.w};
+                    // the target group 0 folds into its exchange-A word, read ahead of
+                    // the MFMAs so that the store does not wait on LDS
+                    const float yv = (DIRECT && gx == 0) ? Yb[tile * 16 + 4 * lq + (li >> 2)] : 0.0f;
                     f4 acc[NUW];
 #pragma unroll
                     for (int u = 0; u < NUW; ++u) acc[u] = f4{0.f, 0.f, 0.f, 0.f};
@@ -485,7 +489,6 @@ __global__ __launch_bounds__(NTHR) void k_train(const TrainArgs a) {
                         // need no targets
                         if ((li & 3) == 0) {
                             const int row = tile * 16 + 4 * lq + (li >> 2);
-                            const float yv = gx == 0 ? Yb[row] : 0.0f;
                             st1(rA, bA + 8u * (uint32_t)(gx * RMAX + row), pack(rowv - yv, tag), true);
                         }
                     } else {
@@ -523,6 +526,35 @@ __global__ __launch_bounds__(NTHR) void k_train(const TrainArgs a) {
 #pragma unroll
                     for (int i = 0; i < RTW; ++i)
                         wa[i] = ld2(rA, bA + 8u * (uint32_t)(peer * RMAX + (wr * RTW + i) * 16 + 4 * lq + 2 * hh));
+                }
+                // the backward's A operands (X rows 4 lq + v, inputs li and li + 16)
+                // come out of LDS while exchange A is in flight
+                float xt[RTW][4][2];
+#pragma unroll
+                for (int i = 0; i < RTW; ++i)
+#pragma unroll
+                    for (int v = 0; v < 4; ++v) {
+                        const float *xr = Xb + ((wr * RTW + i) * 16 + 4 * lq + v) * XS + li;
+                        xt[i][v][0] = xr[0];
+                        xt[i][v][1] = xr[16];
+                    }
+                // deferred loss of the previous step, reduced while exchange A is in
+                // flight: its words are long written, and they stay intact at least
+                // until this workgroup has passed the barrier below (no group-0
+                // workgroup can store the next step's words before every owner of
+                // group 0 has this workgroup's exchange-B words)
+                if (lossw && s > 0) {
+                    wt.settle(sw, tag_prev, [&](int) { return lane < PR ? ld1(rB, sse_prev) : pack(0.f, tag_prev); });
+                    const float sse = sum64(lane < PR ? val_of(sw[0]) : 0.0f);
+                    if (lane == 0) {
+                        const float L = sse / (float)nb_prev;               // eq. 14
+                        float *lo = COLD(loss), *sl = COLD(step_loss), *el = COLD(epoch_loss);
+                        if (lo) lo[0] = L;
+                        if (sl) sl[s - 1] = L;
+                        if (prev.sb == 0) epoch_sse = 0.0;
+                        epoch_sse += (double)sse;
+                        if (el) el[prev.e] = (float)(epoch_sse * (double)COLD(inv_n));
+                    }
                 }
                 f4 pacc[2][NUW];
 #pragma unroll
@@ -577,8 +609,7 @@ __global__ __launch_bounds__(NTHR) void k_train(const TrainArgs a) {
                     // ---- 3. backward: P += X_tile^T (dZ2 (.) mask) ----------------
 #pragma unroll
                     for (int v = 0; v < 4; ++v) {
-                        const float *xr = Xb + (tile * 16 + 4 * lq + v) * XS + li;
-                        const float xt0 = xr[0], xt1 = xr[16];
+                        const float xt0 = xt[i][v][0], xt1 = xt[i][v][1];
 #pragma unroll
                         for (int u = 0; u < NUW; ++u) {
                             const bool on = (mbits >> ((i * NUW + u) * 4 + v)) & 1u;
@@ -602,20 +633,6 @@ __global__ __launch_bounds__(NTHR) void k_train(const TrainArgs a) {
                             make_float4(pacc[kt][u][0], pacc[kt][u][1], pacc[kt][u][2], pacc[kt][u][3]);
                     }
 
-                // deferred loss of the previous step (its words are long written)
-                if (lossw && s > 0) {
-                    wt.settle(sw, tag_prev, [&](int) { return lane < PR ? ld1(rB, sse_prev) : pack(0.f, tag_prev); });
-                    const float sse = sum64(lane < PR ? val_of(sw[0]) : 0.0f);
-                    if (lane == 0) {
-                        const float L = sse / (float)nb_prev;               // eq. 14
-                        float *lo = COLD(loss), *sl = COLD(step_loss), *el = COLD(epoch_loss);
-                        if (lo) lo[0] = L;
-                        if (sl) sl[s - 1] = L;
-                        if (prev.sb == 0) epoch_sse = 0.0;
-                        epoch_sse += (double)sse;
-                        if (el) el[prev.e] = (float)(epoch_sse * (double)COLD(inv_n));
-                    }
-                }
                 __syncthreads();   // P partials and SSE of every wave in LDS
                 TRACE(3);
 
