@@ -14,6 +14,13 @@ Pins (tests/test_oracle_pins.py): central finite differences, the closed form
 of an all-active (linear) net, a hand-worked two-sample step, the strict
 ReLU'(0) = 0 convention, torch float64 autograd at the real shapes, and
 invariants of the batch-size scaling.
+
+``oracle_deep.c`` (its own library, liboracle_deep.so, sharing no code with
+oracle.c) extends the same equations to L hidden layers of width h; the
+``deep_*`` functions below marshal into it. Its pins
+(tests/test_oracle_deep_pins.py): agreement with oracle.c at L = 1, central
+finite differences, the closed form of an all-active deep (linear) net, and
+torch float64 autograd.
 """
 from __future__ import annotations
 
@@ -26,21 +33,31 @@ import numpy as np
 _HERE = os.path.dirname(os.path.abspath(__file__))
 _SRC = os.path.join(_HERE, "oracle.c")
 _LIB = os.path.join(_HERE, "liboracle.so")
+_DEEP_SRC = os.path.join(_HERE, "oracle_deep.c")
+_DEEP_LIB = os.path.join(_HERE, "liboracle_deep.so")
 _lib = None
+_deep_lib = None
 
 _f32p = np.ctypeslib.ndpointer(np.float32, flags="C_CONTIGUOUS")
 _f64p = np.ctypeslib.ndpointer(np.float64, flags="C_CONTIGUOUS")
 _i32p = np.ctypeslib.ndpointer(np.int32, flags="C_CONTIGUOUS")
 
 
+def _gcc(src, lib):
+    tmp = lib + ".tmp%d" % os.getpid()
+    subprocess.check_call(["gcc", "-O2", "-std=c11", "-fPIC", "-shared",
+                           "-ffp-contract=off", "-fno-fast-math", "-Wall",
+                           "-o", tmp, src, "-lm"])
+    os.replace(tmp, lib)
+
+
 def build(force: bool = True) -> str:
-    """Compile liboracle.so with gcc (plain -O2, no FMA contraction, no fast-math)."""
+    """Compile liboracle.so and liboracle_deep.so with gcc (plain -O2, no FMA
+    contraction, no fast-math)."""
     if force or not os.path.exists(_LIB):
-        tmp = _LIB + ".tmp%d" % os.getpid()
-        subprocess.check_call(["gcc", "-O2", "-std=c11", "-fPIC", "-shared",
-                               "-ffp-contract=off", "-fno-fast-math", "-Wall",
-                               "-o", tmp, _SRC, "-lm"])
-        os.replace(tmp, _LIB)
+        _gcc(_SRC, _LIB)
+    if force or not os.path.exists(_DEEP_LIB):
+        _gcc(_DEEP_SRC, _DEEP_LIB)
     return _LIB
 
 
@@ -66,6 +83,34 @@ def _load():
                                      ctypes.POINTER(ctypes.c_int64)]
         _lib = lib
     return _lib
+
+
+def _load_deep():
+    global _deep_lib
+    if _deep_lib is None:
+        if not os.path.exists(_DEEP_LIB):
+            _gcc(_DEEP_SRC, _DEEP_LIB)
+        lib = ctypes.CDLL(_DEEP_LIB)
+        lib.oracle_deep_param_count.restype = ctypes.c_int64
+        lib.oracle_deep_param_count.argtypes = [ctypes.c_int32] * 3
+        lib.oracle_deep_forward.restype = ctypes.c_int
+        lib.oracle_deep_forward.argtypes = [_f32p, ctypes.c_int64, ctypes.c_void_p, ctypes.c_int64,
+                                            ctypes.c_int32, ctypes.c_int32, ctypes.c_int32, _f64p,
+                                            _f64p]
+        lib.oracle_deep_grad.restype = ctypes.c_int
+        lib.oracle_deep_grad.argtypes = [_f32p, _f32p, ctypes.c_int64, ctypes.c_void_p,
+                                         ctypes.c_int64, ctypes.c_int32, ctypes.c_int32,
+                                         ctypes.c_int32, _f64p, _f64p,
+                                         ctypes.POINTER(ctypes.c_double),
+                                         ctypes.POINTER(ctypes.c_double)]
+        lib.oracle_deep_train.restype = ctypes.c_int
+        lib.oracle_deep_train.argtypes = [_f32p, _f32p, ctypes.c_int64, ctypes.c_int32,
+                                          ctypes.c_int32, ctypes.c_int32, _f64p, ctypes.c_int64,
+                                          ctypes.c_double, ctypes.c_int32, ctypes.c_void_p,
+                                          ctypes.c_int64, ctypes.c_void_p, ctypes.c_void_p,
+                                          ctypes.POINTER(ctypes.c_int64)]
+        _deep_lib = lib
+    return _deep_lib
 
 
 def _ptr(a):
@@ -141,6 +186,102 @@ def train(X, Y, W1, W2, batch, lr, epochs, perm=None, max_steps=-1):
         raise ValueError("oracle_train failed: %d" % rc)
     return dict(W1=W1, W2=W2, step_loss=step_loss[:steps.value],
                 epoch_loss=epoch_loss[:epochs], steps=steps.value)
+
+
+# --- L hidden layers (oracle_deep.c) -------------------------------------------
+
+def deep_param_count(d, h, L):
+    return int(_load_deep().oracle_deep_param_count(d, h, L))
+
+
+def deep_split(P, d, h, L):
+    """Views of a flat parameter array: ([W_1, ..., W_L], w_o)."""
+    P = np.asarray(P)
+    Ws, off = [], 0
+    for l in range(L):
+        K = d if l == 0 else h
+        Ws.append(P[off:off + K * h].reshape(K, h))
+        off += K * h
+    return Ws, P[off:off + h]
+
+
+def deep_forward(X, P, d, h, L, idx=None, nb=None):
+    """Ypred (fp64) of the L-hidden-layer net for rows ``idx`` of X."""
+    X = np.ascontiguousarray(X, dtype=np.float32)
+    P = np.ascontiguousarray(P, dtype=np.float64)
+    idx = _idx(idx)
+    if nb is None:
+        nb = X.shape[0] if idx is None else idx.shape[0]
+    out = np.empty(nb, dtype=np.float64)
+    rc = _load_deep().oracle_deep_forward(X, X.shape[0], _ptr(idx), nb, d, h, L, P, out)
+    if rc != 0:
+        raise ValueError("oracle_deep_forward failed: %d" % rc)
+    return out
+
+
+def deep_grad(X, Y, P, d, h, L, idx=None, nb=None):
+    """Gradients of the batch MSE: returns (dP flat fp64, loss, margin), margin =
+    the smallest |Z| / sum |terms| over every pre-activation of the batch."""
+    X = np.ascontiguousarray(X, dtype=np.float32)
+    Y = np.ascontiguousarray(np.reshape(Y, -1), dtype=np.float32)
+    P = np.ascontiguousarray(P, dtype=np.float64)
+    idx = _idx(idx)
+    if nb is None:
+        nb = X.shape[0] if idx is None else idx.shape[0]
+    dP = np.empty_like(P)
+    loss = ctypes.c_double(0.0)
+    margin = ctypes.c_double(0.0)
+    rc = _load_deep().oracle_deep_grad(X, Y, X.shape[0], _ptr(idx), nb, d, h, L, P, dP,
+                                       ctypes.byref(loss), ctypes.byref(margin))
+    if rc != 0:
+        raise ValueError("oracle_deep_grad failed: %d" % rc)
+    return dP, loss.value, margin.value
+
+
+def deep_train(X, Y, P, d, h, L, batch, lr, epochs, perm=None, max_steps=-1):
+    """Mini-batch SGD of the L-hidden-layer net in fp64. Returns dict(P,
+    step_loss, epoch_loss, steps)."""
+    X = np.ascontiguousarray(X, dtype=np.float32)
+    Y = np.ascontiguousarray(np.reshape(Y, -1), dtype=np.float32)
+    P = np.array(P, dtype=np.float64, order="C", copy=True)
+    n = X.shape[0]
+    if perm is not None:
+        perm = np.ascontiguousarray(perm, dtype=np.int32)
+        if perm.shape != (epochs, n):
+            raise ValueError("perm must be [epochs, n]")
+    spe = -(-n // batch)
+    total = spe * epochs if max_steps < 0 else min(max_steps, spe * epochs)
+    step_loss = np.zeros(max(total, 1), dtype=np.float64)
+    epoch_loss = np.zeros(max(epochs, 1), dtype=np.float64)
+    steps = ctypes.c_int64(0)
+    rc = _load_deep().oracle_deep_train(X, Y, n, d, h, L, P, batch, float(lr), epochs,
+                                        _ptr(perm), max_steps, _ptr(step_loss),
+                                        _ptr(epoch_loss), ctypes.byref(steps))
+    if rc != 0:
+        raise ValueError("oracle_deep_train failed: %d" % rc)
+    return dict(P=P, step_loss=step_loss[:steps.value], epoch_loss=epoch_loss[:epochs],
+                steps=steps.value)
+
+
+class swapped_deep_library:
+    """Points the deep_* functions at another build of oracle_deep.c (mutation
+    tests only)."""
+
+    def __init__(self, path):
+        self.path = path
+        self.saved = None
+
+    def __enter__(self):
+        global _deep_lib, _DEEP_LIB
+        self.saved = (_deep_lib, _DEEP_LIB)
+        _deep_lib, _DEEP_LIB = None, self.path
+        _load_deep()
+        return self
+
+    def __exit__(self, *exc):
+        global _deep_lib, _DEEP_LIB
+        _deep_lib, _DEEP_LIB = self.saved
+        return False
 
 
 class swapped_library:
