@@ -224,6 +224,71 @@ def measure_forward(h, X, args, mlp, torch, np):
     }
 
 
+def measure_deep(w, args, mlp, torch, np):
+    """mlp_deep_train_epochs over workload w (L hidden layers): samples/s and the
+    call's algorithmic FLOP/s (every launch of the call, between two events)."""
+    import datagen
+    data = datagen.make_workload(w)
+    dev = torch.device("cuda:0")
+    X = torch.from_numpy(data.X).to(dev)
+    Y = torch.from_numpy(data.Y).to(dev)
+    perm = None if data.perm is None else torch.from_numpy(data.perm).to(dev)
+    P0 = torch.from_numpy(datagen.make_deep_params(w.d_in, w.hidden, w.layers, w.seed)).to(dev)
+    P = P0.clone()
+    ctx = mlp.mlp_deep_init(P, w.hidden, w.layers, w.batch)
+    el = torch.zeros(w.epochs, dtype=torch.float32, device=dev)
+    mlp.mlp_deep_profile(ctx, True)
+
+    def step():
+        P.copy_(P0)
+        mlp.mlp_deep_train_epochs(ctx, X, Y, w.batch, w.lr, w.epochs, perm=perm, epoch_loss=el)
+        return mlp.mlp_deep_last_kernel_ms(ctx)
+
+    for _ in range(args.warmup):
+        step()
+    torch.cuda.synchronize()
+    mlp.mlp_deep_check_errors(ctx)
+    t0 = time.perf_counter()
+    ms = [step() for _ in range(args.steps)]
+    torch.cuda.synchronize()
+    t1 = time.perf_counter()
+    mlp.mlp_deep_check_errors(ctx)
+    samples = w.n * w.epochs
+    flop = float(w.flop_per_sample()) * samples
+    achieved = flop / (float(np.mean(ms)) / 1e3) / 1e12
+    out = {
+        "metric": "training samples/sec (fwd+bwd+SGD), %d hidden layers" % w.layers,
+        "value": samples / ((t1 - t0) / args.steps),
+        "unit": "samples/s",
+        "n_gpus": 1,
+        "steps": args.steps,
+        "warmup": args.warmup,
+        "ms_per_step": (t1 - t0) / args.steps * 1e3,
+        "higher_is_better": True,
+        "dtype": "f32",
+        "data": "synthetic",
+        "config": {"workload": w.name, "d_in": w.d_in, "hidden": w.hidden, "layers": w.layers,
+                   "n": w.n, "batch": w.batch, "lr": w.lr, "epochs": w.epochs,
+                   "sgd_steps": w.steps},
+        "roofline": {"bound": "mfma", "achieved": achieved, "peak": FP32_PEAK_TFLOPS,
+                     "unit": "TFLOP/s", "frac": achieved / FP32_PEAK_TFLOPS,
+                     "kernel_ms": float(np.mean(ms)), "flop_per_launch": flop},
+        "us_per_sgd_step": float(np.mean(ms)) * 1e3 / w.steps,
+        "final_epoch_loss": el.cpu().numpy().tolist(),
+    }
+    if not args.no_cpu_baseline:
+        import oracle
+        n_steps = 1
+        t = time.perf_counter()
+        oracle.deep_train(data.X, data.Y, P0.cpu().numpy(), w.d_in, w.hidden, w.layers, w.batch,
+                          w.lr, w.epochs, perm=data.perm, max_steps=n_steps)
+        dt = time.perf_counter() - t
+        out["cpu_baseline"] = {"value": n_steps * w.batch / dt, "unit": "samples/s", "cores": 1,
+                               "kind": "oracle",
+                               "sample": "first SGD step (%d samples), fp64, one thread" % w.batch}
+    return out
+
+
 def main():
     ap = argparse.ArgumentParser()
     ap.add_argument("--gpus", type=int, default=1)
@@ -231,11 +296,12 @@ def main():
     ap.add_argument("--warmup", type=int, default=2)
     ap.add_argument("--workload", type=int, default=4,
                     help="index into datagen.WORKLOADS (default: the 10M-sample 32-256-1 run)")
-    ap.add_argument("--suite", choices=("configs", "sweep", "table1", "forward"), default=None,
+    ap.add_argument("--suite", choices=("configs", "sweep", "table1", "forward", "deep"),
+                    default=None,
                     help="instead of the one headline line, print one line per workload of a "
                          "suite: the five evaluation workloads, the hidden-width sweep "
-                         "(Table II sizes), the Table I sizes, or mlp_forward over the "
-                         "10M-row dataset at every hidden width")
+                         "(Table II sizes), the Table I sizes, mlp_forward over the "
+                         "10M-row dataset at every hidden width, or the deeper nets")
     ap.add_argument("--strategy", choices=("fused", "tile", "optimized", "baseline"),
                     default="fused",
                     help="training strategy (the paper's baseline and optimized strategies, "
@@ -271,6 +337,10 @@ def main():
         X = torch.from_numpy(data.X).to("cuda:0")
         for h in datagen.SWEEP_HIDDEN:
             print(json.dumps(measure_forward(h, X, args, mlp, torch, np)), flush=True)
+        return
+    if args.suite == "deep":
+        for w in datagen.DEEP:
+            print(json.dumps(measure_deep(w, args, mlp, torch, np)), flush=True)
         return
     suite = datagen.SUITES[args.suite] if args.suite else [datagen.WORKLOADS[args.workload]]
     for w in suite:

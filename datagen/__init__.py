@@ -44,6 +44,7 @@ class Workload:
     shuffle: bool
     seed: int
     d_in: int = D_IN
+    layers: int = 1            # hidden layers of width `hidden`
 
     @property
     def steps_per_epoch(self) -> int:
@@ -64,8 +65,13 @@ class Workload:
         return self.n * self.epochs
 
     def flop_per_sample(self) -> int:
-        """Five contractions at 2 FLOP per multiply-add: 2*(d*h + h + h + h + d*h)."""
-        return 2 * (2 * self.d_in * self.hidden + 3 * self.hidden)
+        """Contractions of one SGD step per sample at 2 FLOP per multiply-add.
+        One hidden layer: 2*(d*h + h + h + h + d*h) (Z1, Ypred, dW2, dZ1, dW1).
+        L layers: forward d*h + (L-1)*h^2 + h, weight gradients the same, the
+        output's back-propagation h, and (L-1)*h^2 for the hidden dH."""
+        d, h, L = self.d_in, self.hidden, self.layers
+        fwd = d * h + (L - 1) * h * h + h
+        return 2 * (2 * fwd + h + (L - 1) * h * h)
 
 
 # The five evaluation workloads. Their seeds are 1000 + k for workload k.
@@ -91,7 +97,13 @@ SWEEP = [Workload("mlp32-%d-1_n2560_b256_e100" % h, h, 2560, 256, 0.002, 100, Tr
 TABLE1 = [Workload("mlp32-256-1_n%d_b256_e100" % n, 256, n, 256, 0.002, 100, True, 3000 + i)
           for i, n in enumerate((256, 2560, 25600))]
 
-SUITES = {"configs": WORKLOADS, "sweep": SWEEP, "table1": TABLE1}
+# Deeper networks (the paper's future work, Sec. VII.B): L hidden layers of
+# width h on the 1M-sample recipe, batch 4096, lr 0.002, one epoch.
+DEEP = [Workload("mlp32-%sx%d-1_n1M_b4096_e1" % (h, L), h, 1_000_000, 4096, 0.002, 1, True,
+                 4000 + 10 * L + h // 64, layers=L)
+        for h, L in ((256, 2), (256, 3), (1024, 2))]
+
+SUITES = {"configs": WORKLOADS, "sweep": SWEEP, "table1": TABLE1, "deep": DEEP}
 
 
 @dataclasses.dataclass
@@ -138,6 +150,19 @@ def make_data(n: int, hidden: int, epochs: int = 1, shuffle: bool = True,
 def make_workload(w: Workload, n: int | None = None) -> Data:
     """Inputs for workload ``w``; ``n`` overrides the sample count (same recipe)."""
     return make_data(w.n if n is None else n, w.hidden, w.epochs, w.shuffle, w.seed, w.d_in)
+
+
+def make_deep_params(d_in: int, hidden: int, layers: int, seed: int) -> np.ndarray:
+    """He-normal parameters of a d_in-h-...-h-1 net in one flat fp32 array:
+    W_1 [d_in x h] (std sqrt(2/d_in)), W_2 .. W_L [h x h] (std sqrt(2/h)), then
+    w_o [h] (std sqrt(2/h))."""
+    r = np.random.Generator(np.random.PCG64(np.random.SeedSequence(seed)))
+    parts = []
+    for l in range(layers):
+        fan_in = d_in if l == 0 else hidden
+        parts.append(r.standard_normal(fan_in * hidden) * math.sqrt(2.0 / fan_in))
+    parts.append(r.standard_normal(hidden) * math.sqrt(2.0 / hidden))
+    return np.concatenate(parts).astype(np.float32)
 
 
 def identity_perm(epochs: int, n: int) -> np.ndarray:

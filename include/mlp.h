@@ -179,6 +179,76 @@ mlp_status mlp_launch_info(mlp_t ctx, int64_t n, int64_t batch, int32_t epochs,
 /* Release the host-side context (the caller still owns every device buffer). */
 void mlp_destroy(mlp_t ctx);
 
+/* ---- Deeper networks: d_in-h-...-h-1 with L hidden layers ----------------------
+ * The paper trains one hidden layer and names deeper networks as future work
+ * (Sec. VII.B). These calls train the same kind of network with L hidden ReLU
+ * layers of width h, by the chain rule of eqs. 11-19 applied layer by layer
+ * (the layer index of eq. 9):
+ *   H_0 = X, H_l = ReLU(H_{l-1} W_l) (l = 1..L), Ypred = H_L w_o,
+ *   L = (1/n_b) sum (Ypred - Y)^2, dZ_o = (2/n_b)(Ypred - Y), dw_o = H_L^T dZ_o,
+ *   dZ_l = dH_l (.) [Z_l > 0], dW_l = H_{l-1}^T dZ_l, dH_{l-1} = dZ_l W_l^T,
+ *   every parameter -= lr * its gradient once all gradients are formed.
+ * With L = 1 the network and its step are those of the calls above.
+ * Parameters live in ONE flat fp32 device array owned by the caller:
+ *   W_1 [d_in x h] row-major (rows = inputs), then W_2 ... W_L, each [h x h]
+ *   row-major (rows = units of the layer below), then w_o [h].
+ * Conventions (device pointers, asynchronous stream semantics, host-side
+ * argument checks that leave parameters untouched, sticky index errors,
+ * bitwise reproducibility, one context per stream) are those of the calls
+ * above. Each SGD step is a sequence of kernel launches from the host (MFMA
+ * GEMMs over the batch's activations in the workspace). */
+typedef struct mlp_deep_ctx *mlp_deep_t;
+
+/* Parameters of a d_in-h-...-h-1 net with `layers` hidden layers:
+ * d_in h + (layers - 1) h^2 + h. 0 for an unsupported shape: d_in must be 32,
+ * hidden a multiple of 64 in [64, 1024], layers in [1, 8]. */
+int64_t mlp_deep_param_count(int32_t d_in, int32_t hidden, int32_t layers);
+
+/* Workspace bytes for batches up to max_batch (the activations of every layer
+ * for max_batch rows, gradient partials, control words); 0 if unsupported.
+ * The workspace must be 256-byte aligned. */
+size_t mlp_deep_workspace_bytes(int32_t d_in, int32_t hidden, int32_t layers, int64_t max_batch);
+
+/* Create a context bound to caller-owned parameters (updated in place by
+ * training calls) and workspace; d_out must be 1. Enqueues a clear of the
+ * control words on `stream`. */
+mlp_status mlp_deep_init(mlp_deep_t *out, int32_t d_in, int32_t hidden, int32_t layers,
+                         int32_t d_out, int64_t max_batch, float *params, void *workspace,
+                         size_t ws_bytes, void *stream);
+
+/* Ypred[t] for rows r_t = idx[t] (idx == NULL: r_t = t), t < B; any B >= 1
+ * (processed max_batch rows at a time). */
+mlp_status mlp_deep_forward(mlp_deep_t ctx, const float *X, int64_t n_rows, const int32_t *idx,
+                            int64_t B, float *Ypred);
+
+/* Gradients of the batch loss at the current parameters into dparams (the
+ * parameter layout, 2/B factor included); loss (nullable) = batch MSE.
+ * 1 <= B <= max_batch. */
+mlp_status mlp_deep_backward(mlp_deep_t ctx, const float *X, int64_t n_rows, const float *Y,
+                             const int32_t *idx, int64_t B, float *dparams, float *loss);
+
+/* One SGD step on the B rows r_t (the gradients of mlp_deep_backward, then
+ * params -= lr * dparams); loss (nullable) = batch MSE before the update. */
+mlp_status mlp_deep_sgd_step(mlp_deep_t ctx, const float *X, int64_t n_rows, const float *Y,
+                             const int32_t *idx, int64_t B, float lr, float *loss);
+
+/* Mini-batch SGD over epochs, with the schedule, permutations, tail batches and
+ * loss outputs of mlp_train_epochs. */
+mlp_status mlp_deep_train_epochs(mlp_deep_t ctx, const float *X, const float *Y, int64_t n,
+                                 int64_t batch, float lr, int32_t epochs, const int32_t *perm,
+                                 int64_t max_steps, float *epoch_loss, float *step_loss);
+
+/* Synchronise and report (then clear) a sticky MLP_ERR_INDEX. */
+mlp_status mlp_deep_check_errors(mlp_deep_t ctx);
+
+/* HIP-event timing of the last mlp_deep_sgd_step / mlp_deep_train_epochs call
+ * (all of its launches), as mlp_profile / mlp_last_kernel_ms. */
+mlp_status mlp_deep_profile(mlp_deep_t ctx, int32_t enable);
+mlp_status mlp_deep_last_kernel_ms(mlp_deep_t ctx, float *ms);
+
+/* Release the host-side context. */
+void mlp_deep_destroy(mlp_deep_t ctx);
+
 /* Static description of a status code. */
 const char *mlp_status_string(mlp_status status);
 

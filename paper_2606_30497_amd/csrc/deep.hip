@@ -1,0 +1,662 @@
+// deep.hip -- mini-batch SGD for a 32-h-...-h-1 ReLU/MSE network with L hidden
+// layers (the deeper networks the paper leaves to future work, Sec. VII.B), on
+// gfx950. The step is the paper's eqs. 11-19 applied layer by layer with the
+// layer index of eq. 9:
+//   H_0 = X_b;  H_l = ReLU(H_{l-1} W_l), l = 1..L;  Ypred = H_L w_o
+//   dZ_o = (2/n_b)(Ypred - Y);  dw_o = H_L^T dZ_o;  G_L = (dZ_o w_o^T) (.) [H_L > 0]
+//   dW_l = H_{l-1}^T G_l;  G_{l-1} = (G_l W_l^T) (.) [H_{l-1} > 0]   (l >= 2)
+//   every parameter -= lr * its gradient, after all gradients are formed.
+// ([H > 0] equals [Z > 0] since H = max(Z, 0), so the pre-activations are never
+// stored.)
+//
+// Unlike the one-layer trainer, the hidden-to-hidden products are real GEMMs
+// ([n_b x h] x [h x h], 2 n_b h^2 FLOP each), so the step is a sequence of
+// MFMA GEMM launches from the host, with the activations of the batch in the
+// workspace:
+//   k_gemm<NN, RELU>   the forward of a layer, ReLU in the epilogue
+//   k_gemm<TN, NONE>   dW_l = H_{l-1}^T G_l, split over row chunks (grid z);
+//                      each chunk writes its own partial, summed in chunk order
+//   k_gemm<NT, MASK>   G_{l-1} = (G_l W_l^T) masked by H_{l-1} > 0
+//   k_deep_out         Ypred, residual, dZ_o and G_L, one wave per row
+//   k_deep_dwo         dw_o partials per row chunk
+//   k_deep_loss        the batch loss, one workgroup, fixed tree
+//   k_deep_apply       sums every gradient's chunk partials in order and
+//                      applies eq. 19 (or writes the gradients)
+// Every output element is one lane's sum in a fixed order, so results are
+// bitwise reproducible.
+//
+// GEMM tile: 64 x 64 outputs per workgroup of four waves (each 32 x 32, 2 x 2
+// v_mfma_f32_16x16x4f32 tiles), K in chunks of 32 staged in LDS k-major with a
+// row stride of 80 floats, so that the 16 lanes reading one MFMA operand row
+// and the next k row fall in different banks; the next chunk's global loads
+// are in flight while the current chunk is computed.
+#include <hip/hip_runtime.h>
+
+#include <math.h>
+#include <new>
+#include <stdint.h>
+#include <string.h>
+
+#include "lanes.h"
+#include "mlp.h"
+#include "mlp_internal.h"
+
+namespace mlp {
+
+constexpr int GT = 64;        // GEMM tile (M and N)
+constexpr int GK = 32;        // K chunk
+constexpr int GLS = 80;       // LDS row stride of a k-major operand tile ([k][m], floats)
+constexpr int GMS = 34;       // LDS row stride of an m-major operand tile ([m][k], floats)
+constexpr int GLDS = GK * GLS;   // floats per operand tile (>= GT * GMS)
+constexpr int SPLIT_MAX = 16; // row chunks of the weight-gradient products
+constexpr int DEEP_MAX_LAYERS = 8;
+
+enum { OP_NN = 0, OP_TN = 1, OP_NT = 2 };
+enum { EP_NONE = 0, EP_RELU = 1, EP_MASK = 2 };
+
+// Global -> register staging of one K chunk: each of the 256 threads holds two
+// float4 of the a tile and two of the b tile.
+struct Stage {
+    float4 a[2], b[2];
+};
+
+template <int OP>
+__device__ __forceinline__ void gemm_fetch(Stage &st, const float *__restrict__ A, int lda,
+                                           const float *__restrict__ B, int ldb, int64_t M, int N,
+                                           int64_t m0, int n0, int64_t k0, int64_t ke, int t) {
+    const float4 z = make_float4(0.f, 0.f, 0.f, 0.f);
+#pragma unroll
+    for (int h = 0; h < 2; ++h) {
+        if constexpr (OP == OP_TN) {              // a(m, k) = A[k lda + m]: float4 along m
+            const int kk = (t >> 4) + 16 * h, mq = (t & 15) * 4;
+            st.a[h] = (k0 + kk < ke && m0 + mq < M)
+                          ? *reinterpret_cast<const float4 *>(A + (k0 + kk) * lda + m0 + mq) : z;
+        } else {                                  // a(m, k) = A[m lda + k]: float4 along k
+            const int row = t >> 2, kq = (t & 3) * 4 + 16 * h;
+            st.a[h] = (m0 + row < M && k0 + kq < ke)
+                          ? *reinterpret_cast<const float4 *>(A + (m0 + row) * lda + k0 + kq) : z;
+        }
+        if constexpr (OP == OP_NT) {              // b(k, n) = B[n ldb + k]: float4 along k
+            const int col = t >> 2, kq = (t & 3) * 4 + 16 * h;
+            st.b[h] = (n0 + col < N && k0 + kq < ke)
+                          ? *reinterpret_cast<const float4 *>(B + (int64_t)(n0 + col) * ldb + k0 + kq)
+                          : z;
+        } else {                                  // b(k, n) = B[k ldb + n]: float4 along n
+            const int kk = (t >> 4) + 16 * h, nq = (t & 15) * 4;
+            st.b[h] = (k0 + kk < ke && n0 + nq < N)
+                          ? *reinterpret_cast<const float4 *>(B + (k0 + kk) * ldb + n0 + nq) : z;
+        }
+    }
+}
+
+// Registers -> LDS. An operand loaded along m (or n) is stored k-major
+// ([k][m], stride GLS); one loaded along k is stored as loaded, m-major
+// ([m][k], stride GMS = 34: the 16 m rows x 2 k columns an MFMA operand read
+// touches per half wave land in 32 distinct banks).
+template <int OP>
+__device__ __forceinline__ void gemm_stash(const Stage &st, float *As, float *Bs, int t) {
+#pragma unroll
+    for (int h = 0; h < 2; ++h) {
+        if constexpr (OP == OP_TN) {
+            *reinterpret_cast<float4 *>(As + ((t >> 4) + 16 * h) * GLS + (t & 15) * 4) = st.a[h];
+        } else {
+            float2 *d = reinterpret_cast<float2 *>(As + (t >> 2) * GMS + (t & 3) * 4 + 16 * h);
+            d[0] = make_float2(st.a[h].x, st.a[h].y);
+            d[1] = make_float2(st.a[h].z, st.a[h].w);
+        }
+        if constexpr (OP == OP_NT) {
+            float2 *d = reinterpret_cast<float2 *>(Bs + (t >> 2) * GMS + (t & 3) * 4 + 16 * h);
+            d[0] = make_float2(st.b[h].x, st.b[h].y);
+            d[1] = make_float2(st.b[h].z, st.b[h].w);
+        } else {
+            *reinterpret_cast<float4 *>(Bs + ((t >> 4) + 16 * h) * GLS + (t & 15) * 4) = st.b[h];
+        }
+    }
+}
+
+// C[m][n] = sum_k a(m, k) b(k, n) over k in [k_begin(z), k_end(z)), where
+//   NN: a(m, k) = A[m lda + k],  b(k, n) = B[k ldb + n]
+//   TN: a(m, k) = A[k lda + m],  b(k, n) = B[k ldb + n]
+//   NT: a(m, k) = A[m lda + k],  b(k, n) = B[n ldb + k]
+// Grid: (ceil(M/64), ceil(N/64), splits); split z covers k in [z kc, min(K, z kc + kc))
+// and writes C + z * c_split. N and the contiguous dimension of every operand
+// are multiples of 16 (hidden widths and d_in); M and K are arbitrary. The next
+// K chunk is loaded into registers while the current one is on the matrix cores.
+template <int OP, int EP>
+__global__ __launch_bounds__(256) void k_gemm(const float *__restrict__ A, int lda,
+                                              const float *__restrict__ B, int ldb,
+                                              float *__restrict__ C, int ldc, int64_t c_split,
+                                              int64_t M, int N, int64_t K, int64_t kc,
+                                              const float *__restrict__ G, int ldg) {
+    __shared__ __attribute__((aligned(16))) float As[GLDS];
+    __shared__ __attribute__((aligned(16))) float Bs[GLDS];
+    const int t = threadIdx.x;
+    const int lane = t & 63, wave = t >> 6;
+    const int li = lane & 15, lq = lane >> 4;
+    const int wm = wave >> 1, wn = wave & 1;
+    const int64_t m0 = (int64_t)blockIdx.x * GT;
+    const int n0 = blockIdx.y * GT;
+    const int64_t kb = (int64_t)blockIdx.z * kc;
+    const int64_t ke = kb + kc < K ? kb + kc : K;
+
+    f4 acc[2][2];
+#pragma unroll
+    for (int i = 0; i < 2; ++i)
+#pragma unroll
+        for (int j = 0; j < 2; ++j) acc[i][j] = f4{0.f, 0.f, 0.f, 0.f};
+
+    Stage st;
+    gemm_fetch<OP>(st, A, lda, B, ldb, M, N, m0, n0, kb, ke, t);
+    for (int64_t k0 = kb; k0 < ke; k0 += GK) {
+        gemm_stash<OP>(st, As, Bs, t);
+        __syncthreads();
+        if (k0 + GK < ke) gemm_fetch<OP>(st, A, lda, B, ldb, M, N, m0, n0, k0 + GK, ke, t);
+        // eight k steps of 4 on the matrix cores
+#pragma unroll
+        for (int ks = 0; ks < GK / 4; ++ks) {
+            const int kr = ks * 4 + lq;
+            float a[2], b[2];
+#pragma unroll
+            for (int i = 0; i < 2; ++i) {
+                const int m = wm * 32 + i * 16 + li;
+                a[i] = OP == OP_TN ? As[kr * GLS + m] : As[m * GMS + kr];
+            }
+#pragma unroll
+            for (int j = 0; j < 2; ++j) {
+                const int n = wn * 32 + j * 16 + li;
+                b[j] = OP == OP_NT ? Bs[n * GMS + kr] : Bs[kr * GLS + n];
+            }
+#pragma unroll
+            for (int i = 0; i < 2; ++i)
+#pragma unroll
+                for (int j = 0; j < 2; ++j)
+                    acc[i][j] = __builtin_amdgcn_mfma_f32_16x16x4f32(a[i], b[j], acc[i][j], 0, 0, 0);
+        }
+        __syncthreads();
+    }
+    // ---- epilogue: lane holds C[4 lq + v][li] of each 16 x 16 tile ----
+    float *Cz = C + (int64_t)blockIdx.z * c_split;
+#pragma unroll
+    for (int i = 0; i < 2; ++i)
+#pragma unroll
+        for (int j = 0; j < 2; ++j) {
+            const int n = n0 + wn * 32 + j * 16 + li;
+#pragma unroll
+            for (int v = 0; v < 4; ++v) {
+                const int64_t m = m0 + wm * 32 + i * 16 + 4 * lq + v;
+                if (m >= M || n >= N) continue;
+                float r = acc[i][j][v];
+                if constexpr (EP == EP_RELU) r = r > 0.0f ? r : 0.0f;           // eq. 12
+                if constexpr (EP == EP_MASK) r = G[m * ldg + n] > 0.0f ? r : 0.0f; // eq. 17
+                Cz[m * ldc + n] = r;
+            }
+        }
+}
+
+// Xb[t][k] = X[r_t][k], Yb[t] = Y[r_t], r_t = idx[off + t] (or off + t);
+// out-of-range rows read row 0 and raise the sticky error.
+__global__ __launch_bounds__(256) void k_deep_gather(const float *__restrict__ X,
+                                                     const float *__restrict__ Y, int64_t n_rows,
+                                                     const int32_t *__restrict__ idx, int64_t off,
+                                                     int64_t nb, float *__restrict__ Xb,
+                                                     float *__restrict__ Yb, int32_t *err) {
+    const int64_t e = (int64_t)blockIdx.x * 256 + threadIdx.x;
+    if (e >= nb * (D_IN / 4)) return;
+    const int64_t t = e / (D_IN / 4);
+    const int q = (int)(e % (D_IN / 4));
+    int64_t r = idx ? (int64_t)idx[off + t] : off + t;
+    if (r < 0 || r >= n_rows) {
+        __hip_atomic_store(err, (int32_t)MLP_ERR_INDEX, __ATOMIC_RELAXED, __HIP_MEMORY_SCOPE_AGENT);
+        r = 0;
+    }
+    reinterpret_cast<float4 *>(Xb)[t * (D_IN / 4) + q] =
+        reinterpret_cast<const float4 *>(X)[r * (D_IN / 4) + q];
+    if (q == 0) Yb[t] = Y ? Y[r] : 0.0f;
+}
+
+// One wave per row: Ypred = H_L w_o (eq. 13); for training also the residual,
+// dZ_o = (2/n_b) r (eq. 15), r^2, and G_L = dZ_o w_o^T (.) [H_L > 0] (eq. 17).
+template <bool TRAIN>
+__global__ __launch_bounds__(256) void k_deep_out(const float *__restrict__ H, int h,
+                                                  const float *__restrict__ wo,
+                                                  const float *__restrict__ Yb, int64_t nb,
+                                                  float scale, float *__restrict__ ypred,
+                                                  float *__restrict__ dz, float *__restrict__ sq,
+                                                  float *__restrict__ Gout) {
+    const int lane = threadIdx.x & 63;
+    const int64_t r = (int64_t)blockIdx.x * 4 + (threadIdx.x >> 6);
+    if (r >= nb) return;
+    const float *hr = H + r * h;
+    float s = 0.0f;
+    for (int j = lane; j < h; j += 64) s = fmaf(hr[j], wo[j], s);
+    s = sum64(s);
+    if (!TRAIN) {
+        if (lane == 0) ypred[r] = s;
+        return;
+    }
+    const float res = s - Yb[r];
+    const float g = scale * res;
+    if (lane == 0) {
+        dz[r] = g;
+        sq[r] = res * res;
+    }
+    float *gr = Gout + r * h;
+    for (int j = lane; j < h; j += 64) gr[j] = hr[j] > 0.0f ? g * wo[j] : 0.0f;
+}
+
+// dw_o partial of row chunk z (eq. 16): part[z][j] = sum over the chunk's rows
+// of H_L[r][j] dZ_o[r]. A workgroup covers 16 units with 16 row phases (thread
+// (p, u): unit 16 bx + u, rows rb + p, rb + p + 16, ... ascending); the 16
+// phase sums meet in LDS and are added in phase order.
+__global__ __launch_bounds__(256) void k_deep_dwo(const float *__restrict__ H, int h,
+                                                  const float *__restrict__ dz, int64_t nb,
+                                                  int64_t kc, float *__restrict__ part,
+                                                  int64_t p_split) {
+    __shared__ float ps[16][17];
+    const int u = threadIdx.x & 15, ph = threadIdx.x >> 4;
+    const int j = blockIdx.x * 16 + u;
+    const int64_t rb = (int64_t)blockIdx.y * kc;
+    const int64_t re = rb + kc < nb ? rb + kc : nb;
+    float s = 0.0f;
+    if (j < h)
+        for (int64_t r = rb + ph; r < re; r += 16) s = fmaf(H[r * h + j], dz[r], s);
+    ps[ph][u] = s;
+    __syncthreads();
+    if (ph == 0 && j < h) {
+        float tot = 0.0f;
+#pragma unroll
+        for (int q = 0; q < 16; ++q) tot += ps[q][u];
+        part[(int64_t)blockIdx.y * p_split + j] = tot;
+    }
+}
+
+// Batch loss (eq. 14): one workgroup, thread i sums rows i, i + 256, ... then a
+// fixed binary tree; step and epoch loss as in the one-layer paths.
+__global__ __launch_bounds__(256) void k_deep_loss(const float *__restrict__ sq, int64_t nb,
+                                                   ReduceArgs a) {
+    __shared__ float part[256];
+    const int i = threadIdx.x;
+    float s = 0.0f;
+    for (int64_t t = i; t < nb; t += 256) s += sq[t];
+    part[i] = s;
+    __syncthreads();
+    for (int w = 128; w >= 1; w >>= 1) {
+        if (i < w) part[i] += part[i + w];
+        __syncthreads();
+    }
+    if (i == 0) {
+        const float sse = part[0];
+        const float L = sse * a.inv_nb;
+        if (a.loss) a.loss[0] = L;
+        if (a.step_loss) a.step_loss[a.step] = L;
+        if (a.epoch_loss) {
+            double acc = a.first_in_epoch ? 0.0 : a.ctl->epoch_sse;
+            acc += (double)sse;
+            a.ctl->epoch_sse = acc;
+            a.epoch_loss[a.epoch] = (float)(acc * a.inv_n);
+        }
+    }
+}
+
+// Row-chunk split of each parameter segment's gradient (W_1 .. W_L, then w_o).
+struct SplitPlan {
+    int nseg;
+    int64_t seg_end[DEEP_MAX_LAYERS + 1];   // exclusive end of segment s in the flat array
+    int splits[DEEP_MAX_LAYERS + 1];        // row chunks (partials) of segment s
+    int64_t kc[DEEP_MAX_LAYERS + 1];        // rows per chunk
+};
+
+// Sum the chunk partials of every parameter's gradient in chunk order, then
+// eq. 19 (sgd) or write the gradient.
+__global__ __launch_bounds__(256) void k_deep_apply(const float *__restrict__ part, SplitPlan sp,
+                                                    int64_t np, float *__restrict__ params,
+                                                    float *__restrict__ dparams, float lr, int sgd) {
+    const int64_t p = (int64_t)blockIdx.x * 256 + threadIdx.x;
+    if (p >= np) return;
+    int seg = 0;
+    while (seg + 1 < sp.nseg && p >= sp.seg_end[seg]) ++seg;
+    float s = 0.0f;
+    for (int z = 0; z < sp.splits[seg]; ++z) s += part[(int64_t)z * np + p];
+    if (sgd) params[p] -= lr * s;
+    else dparams[p] = s;
+}
+
+// ---------------------------------------------------------------------------
+// Host side
+// ---------------------------------------------------------------------------
+
+struct DeepCtx {
+    int hidden = 0, layers = 0;
+    int64_t max_batch = 0, np = 0;
+    float *params = nullptr;
+    Control *ctl = nullptr;
+    float *Xb = nullptr, *Yb = nullptr, *dz = nullptr, *sq = nullptr, *yp = nullptr;
+    float *H = nullptr;       // [layers][max_batch x hidden]
+    float *G[2] = {nullptr, nullptr};
+    float *part = nullptr;    // [SPLIT_MAX][np]
+    hipStream_t stream = nullptr;
+    bool profile = false, ev_valid = false;
+    hipEvent_t ev0 = nullptr, ev1 = nullptr;
+};
+
+static int64_t deep_np(int h, int L) { return (int64_t)D_IN * h + (int64_t)(L - 1) * h * h + h; }
+static int64_t layer_offset(int h, int l) {   // W_l, l = 1..L; w_o at l = L + 1
+    return l == 1 ? 0 : (int64_t)D_IN * h + (int64_t)(l - 2) * h * h;
+}
+static size_t pad64f(size_t n) { return (n + 63) / 64 * 64; }
+
+static bool deep_shape_ok(int32_t d_in, int32_t hidden, int32_t layers) {
+    return d_in == D_IN && hidden >= 64 && hidden <= 1024 && hidden % 64 == 0 && layers >= 1 &&
+           layers <= DEEP_MAX_LAYERS;
+}
+
+static size_t deep_ws_floats(int h, int L, int64_t mb) {
+    const size_t b = (size_t)mb;
+    return pad64f(CTL_BYTES / 4) + pad64f(b * D_IN) + 4 * pad64f(b) +
+           (size_t)(L + 2) * pad64f(b * (size_t)h) + (size_t)SPLIT_MAX * pad64f((size_t)deep_np(h, L));
+}
+
+// Row chunks of the weight-gradient products for a batch of nb rows: enough
+// chunks that a segment's workgroups (output tiles x chunks) reach about 512,
+// at most SPLIT_MAX, and at least 64 rows per chunk.
+static void split_plan(int h, int L, int64_t nb, SplitPlan *sp) {
+    sp->nseg = L + 1;
+    for (int s = 0; s <= L; ++s) {
+        // segment s < L: W_{s+1}, tiles of 64 x 64 over [K x h]; s = L: w_o, 16 units a workgroup
+        const int64_t K = s == 0 ? D_IN : h;
+        const int64_t tiles = s < L ? ((K + GT - 1) / GT) * (h / GT) : h / 16;
+        int splits = (int)((512 + tiles - 1) / tiles);
+        const int64_t by_rows = (nb + 63) / 64;
+        if (splits > by_rows) splits = (int)by_rows;
+        splits = splits < 1 ? 1 : (splits > SPLIT_MAX ? SPLIT_MAX : splits);
+        int64_t c = (nb + splits - 1) / splits;
+        c = (c + GK - 1) / GK * GK;
+        sp->kc[s] = c;
+        sp->splits[s] = (int)((nb + c - 1) / c);
+        sp->seg_end[s] = s < L ? layer_offset(h, s + 2) : deep_np(h, L);
+    }
+}
+
+template <int OP, int EP>
+static hipError_t gemm(hipStream_t st, const float *A, int lda, const float *B, int ldb, float *C,
+                       int ldc, int64_t c_split, int64_t M, int N, int64_t K, int splits,
+                       int64_t kc, const float *G = nullptr, int ldg = 0) {
+    const dim3 grid((unsigned)((M + GT - 1) / GT), (unsigned)((N + GT - 1) / GT), (unsigned)splits);
+    hipLaunchKernelGGL((k_gemm<OP, EP>), grid, dim3(256), 0, st, A, lda, B, ldb, C, ldc, c_split, M,
+                       N, K, kc, G, ldg);
+    return hipGetLastError();
+}
+
+#define DEEP_TRY(x)                        \
+    do {                                   \
+        hipError_t e_ = (x);               \
+        if (e_ != hipSuccess) return e_;   \
+    } while (0)
+
+static unsigned blocks_of(int64_t n, int per) { return (unsigned)((n + per - 1) / per); }
+
+// Forward of nb gathered rows (Xb) through every hidden layer into c.H.
+static hipError_t deep_forward_layers(const DeepCtx &c, int64_t nb) {
+    const int h = c.hidden;
+    const float *in = c.Xb;
+    int K = D_IN;
+    for (int l = 1; l <= c.layers; ++l) {
+        float *out = c.H + (int64_t)(l - 1) * c.max_batch * h;
+        DEEP_TRY((gemm<OP_NN, EP_RELU>(c.stream, in, K, c.params + layer_offset(h, l), h, out, h,
+                                       0, nb, h, K, 1, K)));
+        in = out;
+        K = h;
+    }
+    return hipSuccess;
+}
+
+// One step (or one gradient evaluation) on batch rows [off, off + nb) of idx.
+static hipError_t deep_step(DeepCtx &c, const float *X, int64_t n_rows, const float *Y,
+                            const int32_t *idx, int64_t off, int64_t nb, const ReduceArgs &ra,
+                            float *dparams) {
+    const int h = c.hidden, L = c.layers;
+    const int64_t mbh = c.max_batch * h;
+    hipLaunchKernelGGL(k_deep_gather, dim3(blocks_of(nb * (D_IN / 4), 256)), dim3(256), 0, c.stream,
+                       X, Y, n_rows, idx, off, nb, c.Xb, c.Yb, &c.ctl->err);
+    DEEP_TRY(hipGetLastError());
+    DEEP_TRY(deep_forward_layers(c, nb));
+    const float *HL = c.H + (int64_t)(L - 1) * mbh;
+    const float *wo = c.params + layer_offset(h, L + 1);
+    int cur = 0;
+    hipLaunchKernelGGL((k_deep_out<true>), dim3(blocks_of(nb, 4)), dim3(256), 0, c.stream, HL, h, wo,
+                       c.Yb, nb, 2.0f / (float)nb, nullptr, c.dz, c.sq, c.G[cur]);
+    DEEP_TRY(hipGetLastError());
+    hipLaunchKernelGGL(k_deep_loss, dim3(1), dim3(256), 0, c.stream, c.sq, nb, ra);
+    DEEP_TRY(hipGetLastError());
+    SplitPlan sp;
+    split_plan(h, L, nb, &sp);
+    hipLaunchKernelGGL(k_deep_dwo, dim3(blocks_of(h, 16), sp.splits[L]), dim3(256), 0, c.stream, HL,
+                       h, c.dz, nb, sp.kc[L], c.part + layer_offset(h, L + 1), c.np);
+    DEEP_TRY(hipGetLastError());
+    for (int l = L; l >= 1; --l) {
+        const int K = l == 1 ? D_IN : h;
+        const float *Hin = l == 1 ? c.Xb : c.H + (int64_t)(l - 2) * mbh;
+        // dW_l = H_{l-1}^T G_l, eq. 18, split over row chunks
+        DEEP_TRY((gemm<OP_TN, EP_NONE>(c.stream, Hin, K, c.G[cur], h, c.part + layer_offset(h, l), h,
+                                       c.np, K, h, nb, sp.splits[l - 1], sp.kc[l - 1])));
+        if (l > 1) {
+            // G_{l-1} = (G_l W_l^T) (.) [H_{l-1} > 0], eq. 17 one layer down
+            DEEP_TRY((gemm<OP_NT, EP_MASK>(c.stream, c.G[cur], h, c.params + layer_offset(h, l), h,
+                                           c.G[cur ^ 1], h, 0, nb, h, h, 1, h, Hin, h)));
+            cur ^= 1;
+        }
+    }
+    hipLaunchKernelGGL(k_deep_apply, dim3(blocks_of(c.np, 256)), dim3(256), 0, c.stream, c.part,
+                       sp, c.np, c.params, dparams, ra.lr, ra.sgd);
+    return hipGetLastError();
+}
+
+}  // namespace mlp
+
+using namespace mlp;
+
+struct mlp_deep_ctx : mlp::DeepCtx {};
+
+extern "C" int64_t mlp_deep_param_count(int32_t d_in, int32_t hidden, int32_t layers) {
+    if (!deep_shape_ok(d_in, hidden, layers)) return 0;
+    return deep_np(hidden, layers);
+}
+
+extern "C" size_t mlp_deep_workspace_bytes(int32_t d_in, int32_t hidden, int32_t layers,
+                                           int64_t max_batch) {
+    if (!deep_shape_ok(d_in, hidden, layers) || max_batch < 1 || max_batch > MLP_MAX_BATCH) return 0;
+    return sizeof(float) * deep_ws_floats(hidden, layers, max_batch);
+}
+
+extern "C" mlp_status mlp_deep_init(mlp_deep_t *out, int32_t d_in, int32_t hidden, int32_t layers,
+                                    int32_t d_out, int64_t max_batch, float *params,
+                                    void *workspace, size_t ws_bytes, void *stream) {
+    if (!out || !params || !workspace) return MLP_ERR_INVALID_ARG;
+    if (!deep_shape_ok(d_in, hidden, layers) || d_out != 1) return MLP_ERR_UNSUPPORTED;
+    if (max_batch < 1 || max_batch > MLP_MAX_BATCH) return MLP_ERR_INVALID_ARG;
+    if (ws_bytes < mlp_deep_workspace_bytes(d_in, hidden, layers, max_batch) ||
+        ((uintptr_t)workspace & 255u))
+        return MLP_ERR_WORKSPACE;
+    mlp_deep_ctx *c = new (std::nothrow) mlp_deep_ctx();
+    if (!c) return MLP_ERR_HIP;
+    c->hidden = hidden;
+    c->layers = layers;
+    c->max_batch = max_batch;
+    c->np = deep_np(hidden, layers);
+    c->params = params;
+    c->stream = (hipStream_t)stream;
+    float *p = (float *)workspace;
+    auto take = [&](size_t n) {
+        float *q = p;
+        p += pad64f(n);
+        return q;
+    };
+    const size_t b = (size_t)max_batch, bh = b * (size_t)hidden;
+    c->ctl = (Control *)take(CTL_BYTES / 4);
+    c->Xb = take(b * D_IN);
+    c->Yb = take(b);
+    c->dz = take(b);
+    c->sq = take(b);
+    c->yp = take(b);
+    c->H = p;
+    p += (size_t)layers * pad64f(bh);
+    c->G[0] = take(bh);
+    c->G[1] = take(bh);
+    c->part = take((size_t)SPLIT_MAX * (size_t)c->np);
+    Ctx tmp;
+    tmp.ctl = c->ctl;
+    tmp.stream = c->stream;
+    if (clear_control(tmp) != hipSuccess) {
+        delete c;
+        return MLP_ERR_HIP;
+    }
+    *out = c;
+    return MLP_OK;
+}
+
+extern "C" void mlp_deep_destroy(mlp_deep_t c) {
+    if (!c) return;
+    if (c->ev0) (void)hipEventDestroy(c->ev0);
+    if (c->ev1) (void)hipEventDestroy(c->ev1);
+    delete c;
+}
+
+static mlp_status deep_status(hipError_t e) { return e == hipSuccess ? MLP_OK : MLP_ERR_HIP; }
+
+extern "C" mlp_status mlp_deep_forward(mlp_deep_t c, const float *X, int64_t n_rows,
+                                       const int32_t *idx, int64_t B, float *Ypred) {
+    if (!c || !X || !Ypred || B < 1 || n_rows < 1) return MLP_ERR_INVALID_ARG;
+    if (!idx && B > n_rows) return MLP_ERR_INVALID_ARG;
+    const int h = c->hidden;
+    const float *HL = c->H + (int64_t)(c->layers - 1) * c->max_batch * h;
+    const float *wo = c->params + layer_offset(h, c->layers + 1);
+    for (int64_t off = 0; off < B; off += c->max_batch) {
+        const int64_t nb = B - off < c->max_batch ? B - off : c->max_batch;
+        hipLaunchKernelGGL(k_deep_gather, dim3(blocks_of(nb * (D_IN / 4), 256)), dim3(256), 0,
+                           c->stream, X, nullptr, n_rows, idx, off, nb, c->Xb, c->Yb, &c->ctl->err);
+        if (hipGetLastError() != hipSuccess) return MLP_ERR_HIP;
+        if (deep_forward_layers(*c, nb) != hipSuccess) return MLP_ERR_HIP;
+        hipLaunchKernelGGL((k_deep_out<false>), dim3(blocks_of(nb, 4)), dim3(256), 0, c->stream, HL,
+                           h, wo, nullptr, nb, 0.0f, Ypred + off, nullptr, nullptr, nullptr);
+        if (hipGetLastError() != hipSuccess) return MLP_ERR_HIP;
+    }
+    return MLP_OK;
+}
+
+static ReduceArgs deep_args(const mlp_deep_ctx *c, int64_t nb) {
+    ReduceArgs a;
+    memset(&a, 0, sizeof(a));
+    a.inv_nb = (float)(1.0 / (double)nb);
+    a.ctl = c->ctl;
+    return a;
+}
+
+extern "C" mlp_status mlp_deep_backward(mlp_deep_t c, const float *X, int64_t n_rows,
+                                        const float *Y, const int32_t *idx, int64_t B,
+                                        float *dparams, float *loss) {
+    if (!c || !X || !Y || !dparams || B < 1 || B > c->max_batch || n_rows < 1)
+        return MLP_ERR_INVALID_ARG;
+    if (!idx && B > n_rows) return MLP_ERR_INVALID_ARG;
+    ReduceArgs a = deep_args(c, B);
+    a.sgd = 0;
+    a.loss = loss;
+    return deep_status(deep_step(*c, X, n_rows, Y, idx, 0, B, a, dparams));
+}
+
+static void deep_prof(mlp_deep_ctx *c, bool begin) {
+    if (!c->profile) return;
+    if (begin) {
+        if (!c->ev0) (void)hipEventCreate(&c->ev0);
+        if (!c->ev1) (void)hipEventCreate(&c->ev1);
+        (void)hipEventRecord(c->ev0, c->stream);
+    } else {
+        (void)hipEventRecord(c->ev1, c->stream);
+        c->ev_valid = true;
+    }
+}
+
+extern "C" mlp_status mlp_deep_sgd_step(mlp_deep_t c, const float *X, int64_t n_rows,
+                                        const float *Y, const int32_t *idx, int64_t B, float lr,
+                                        float *loss) {
+    if (!c || !X || !Y || B < 1 || B > c->max_batch || n_rows < 1 || !isfinite(lr))
+        return MLP_ERR_INVALID_ARG;
+    if (!idx && B > n_rows) return MLP_ERR_INVALID_ARG;
+    ReduceArgs a = deep_args(c, B);
+    a.sgd = 1;
+    a.lr = lr;
+    a.loss = loss;
+    deep_prof(c, true);
+    const mlp_status st = deep_status(deep_step(*c, X, n_rows, Y, idx, 0, B, a, nullptr));
+    deep_prof(c, false);
+    return st;
+}
+
+extern "C" mlp_status mlp_deep_train_epochs(mlp_deep_t c, const float *X, const float *Y,
+                                            int64_t n, int64_t batch, float lr, int32_t epochs,
+                                            const int32_t *perm, int64_t max_steps,
+                                            float *epoch_loss, float *step_loss) {
+    if (!c || !X || !Y || n < 1 || batch < 1 || batch > c->max_batch || epochs < 1 ||
+        !isfinite(lr) || max_steps < -1)
+        return MLP_ERR_INVALID_ARG;
+    if ((int64_t)epochs * n > ((int64_t)1 << 40)) return MLP_ERR_INVALID_ARG;
+    Ctx tmp;
+    tmp.stream = c->stream;
+    hipError_t e = hipSuccess;
+    if (epoch_loss) e = fill(tmp, epoch_loss, epochs, 0.0f);
+    if (e != hipSuccess) return MLP_ERR_HIP;
+    const int64_t spe = (n + batch - 1) / batch;
+    int64_t step = 0;
+    deep_prof(c, true);
+    for (int32_t ep = 0; ep < epochs && e == hipSuccess; ++ep) {
+        for (int64_t s = 0; s < spe; ++s) {
+            if (max_steps >= 0 && step >= max_steps) break;
+            const int64_t off = s * batch;
+            const int64_t nb = n - off < batch ? n - off : batch;
+            ReduceArgs a = deep_args(c, nb);
+            a.sgd = 1;
+            a.lr = lr;
+            a.inv_n = (float)(1.0 / (double)n);
+            a.step_loss = step_loss;
+            a.step = step;
+            a.epoch_loss = epoch_loss;
+            a.epoch = ep;
+            a.first_in_epoch = s == 0;
+            const int32_t *ix = perm ? perm + (int64_t)ep * n : nullptr;
+            e = deep_step(*c, X, n, Y, ix, off, nb, a, nullptr);
+            if (e != hipSuccess) break;
+            ++step;
+        }
+    }
+    deep_prof(c, false);
+    return deep_status(e);
+}
+
+extern "C" mlp_status mlp_deep_check_errors(mlp_deep_t c) {
+    if (!c) return MLP_ERR_INVALID_ARG;
+    if (hipStreamSynchronize(c->stream) != hipSuccess) return MLP_ERR_HIP;
+    int32_t err = 0;
+    if (hipMemcpy(&err, &c->ctl->err, sizeof(err), hipMemcpyDeviceToHost) != hipSuccess)
+        return MLP_ERR_HIP;
+    if (err) {
+        Ctx tmp;
+        tmp.ctl = c->ctl;
+        tmp.stream = c->stream;
+        if (clear_control(tmp) != hipSuccess || hipStreamSynchronize(c->stream) != hipSuccess)
+            return MLP_ERR_HIP;
+        return MLP_ERR_INDEX;
+    }
+    return MLP_OK;
+}
+
+extern "C" mlp_status mlp_deep_profile(mlp_deep_t c, int32_t enable) {
+    if (!c) return MLP_ERR_INVALID_ARG;
+    c->profile = enable != 0;
+    c->ev_valid = false;
+    return MLP_OK;
+}
+
+extern "C" mlp_status mlp_deep_last_kernel_ms(mlp_deep_t c, float *ms) {
+    if (!c || !ms || !c->ev_valid) return MLP_ERR_INVALID_ARG;
+    if (hipEventSynchronize(c->ev1) != hipSuccess) return MLP_ERR_HIP;
+    return deep_status(hipEventElapsedTime(ms, c->ev0, c->ev1));
+}

@@ -30,7 +30,11 @@ STRATEGIES = {"fused": STRATEGY_FUSED, "tile": STRATEGY_TILE, "optimized": STRAT
 EXPORTS = ("mlp_workspace_bytes", "mlp_init", "mlp_set_stream", "mlp_strategy_workspace_bytes",
            "mlp_set_strategy", "mlp_forward", "mlp_backward",
            "mlp_sgd_step", "mlp_train_epochs", "mlp_check_errors", "mlp_profile",
-           "mlp_last_kernel_ms", "mlp_launch_info", "mlp_destroy", "mlp_status_string")
+           "mlp_last_kernel_ms", "mlp_launch_info", "mlp_destroy", "mlp_status_string",
+           "mlp_deep_param_count", "mlp_deep_workspace_bytes", "mlp_deep_init", "mlp_deep_forward",
+           "mlp_deep_backward", "mlp_deep_sgd_step", "mlp_deep_train_epochs",
+           "mlp_deep_check_errors", "mlp_deep_profile", "mlp_deep_last_kernel_ms",
+           "mlp_deep_destroy")
 
 
 class MLPError(RuntimeError):
@@ -81,6 +85,19 @@ def load(require_built: bool = True):
                                            ctypes.POINTER(_i64)]),
         "mlp_destroy": (None, [_vp]),
         "mlp_status_string": (ctypes.c_char_p, [ctypes.c_int]),
+        "mlp_deep_param_count": (_i64, [_i32, _i32, _i32]),
+        "mlp_deep_workspace_bytes": (ctypes.c_size_t, [_i32, _i32, _i32, _i64]),
+        "mlp_deep_init": (ctypes.c_int, [ctypes.POINTER(_vp), _i32, _i32, _i32, _i32, _i64, _vp,
+                                         _vp, ctypes.c_size_t, _vp]),
+        "mlp_deep_forward": (ctypes.c_int, [_vp, _vp, _i64, _vp, _i64, _vp]),
+        "mlp_deep_backward": (ctypes.c_int, [_vp, _vp, _i64, _vp, _vp, _i64, _vp, _vp]),
+        "mlp_deep_sgd_step": (ctypes.c_int, [_vp, _vp, _i64, _vp, _vp, _i64, _f32, _vp]),
+        "mlp_deep_train_epochs": (ctypes.c_int, [_vp, _vp, _vp, _i64, _i64, _f32, _i32, _vp, _i64,
+                                                 _vp, _vp]),
+        "mlp_deep_check_errors": (ctypes.c_int, [_vp]),
+        "mlp_deep_profile": (ctypes.c_int, [_vp, _i32]),
+        "mlp_deep_last_kernel_ms": (ctypes.c_int, [_vp, ctypes.POINTER(_f32)]),
+        "mlp_deep_destroy": (None, [_vp]),
     }
     for name, (res, args) in sig.items():
         f = getattr(lib, name)
@@ -256,3 +273,113 @@ def mlp_launch_info(ctx: Context, n, batch, epochs):
 
 def mlp_status_string(status: int) -> str:
     return load().mlp_status_string(status).decode()
+
+
+# --- deeper networks (L hidden layers) ------------------------------------------
+
+def mlp_deep_param_count(d_in: int, hidden: int, layers: int) -> int:
+    return int(load().mlp_deep_param_count(d_in, hidden, layers))
+
+
+class DeepContext:
+    """A deep-net context bound to caller-owned parameters and workspace."""
+
+    def __init__(self, handle, params, workspace, hidden, layers, max_batch):
+        self.handle = handle
+        self.params, self.workspace = params, workspace
+        self.hidden, self.layers, self.max_batch = hidden, layers, max_batch
+
+    def __del__(self):
+        h, self.handle = getattr(self, "handle", None), None
+        if h and _lib is not None:
+            _lib.mlp_deep_destroy(h)
+
+
+def mlp_deep_init(params: torch.Tensor, hidden: int, layers: int, max_batch: int,
+                  workspace=None, stream=None) -> DeepContext:
+    """params: flat fp32 [W_1 (32 x h) | W_2 .. W_L (h x h) | w_o (h)], updated in place."""
+    lib = load()
+    np_ = lib.mlp_deep_param_count(D_IN, hidden, layers)
+    if np_ == 0:
+        raise MLPError("mlp_deep_param_count", -2)
+    _dev(params, "params", numel=np_)
+    need = lib.mlp_deep_workspace_bytes(D_IN, hidden, layers, max_batch)
+    if need == 0:
+        raise MLPError("mlp_deep_workspace_bytes", -1)
+    if workspace is None:
+        workspace = torch.empty(need, dtype=torch.uint8, device=params.device)
+    _dev(workspace, "workspace", dtype=torch.uint8, numel=need)
+    if stream is None:
+        stream = torch.cuda.current_stream(params.device).cuda_stream
+    handle = _vp()
+    _check("mlp_deep_init", lib.mlp_deep_init(ctypes.byref(handle), D_IN, hidden, layers, 1,
+                                              max_batch, params.data_ptr(), workspace.data_ptr(),
+                                              workspace.numel(), stream))
+    return DeepContext(handle, params, workspace, hidden, layers, max_batch)
+
+
+def mlp_deep_forward(ctx: DeepContext, X, idx=None, B=None, out=None):
+    n_rows = X.shape[0]
+    B = (n_rows if idx is None else idx.numel()) if B is None else B
+    _dev(X, "X", numel=n_rows * D_IN)
+    if out is None:
+        out = torch.empty(B, dtype=torch.float32, device=X.device)
+    _check("mlp_deep_forward", load().mlp_deep_forward(ctx.handle, X.data_ptr(), n_rows,
+                                                       _rows(idx, B), B,
+                                                       _dev(out, "Ypred", numel=B)))
+    return out
+
+
+def mlp_deep_backward(ctx: DeepContext, X, Y, idx=None, B=None):
+    n_rows = X.shape[0]
+    B = (n_rows if idx is None else idx.numel()) if B is None else B
+    _dev(X, "X", numel=n_rows * D_IN)
+    _dev(Y, "Y", numel=n_rows)
+    dP = torch.empty_like(ctx.params)
+    loss = torch.empty(1, dtype=torch.float32, device=X.device)
+    _check("mlp_deep_backward", load().mlp_deep_backward(ctx.handle, X.data_ptr(), n_rows,
+                                                         Y.data_ptr(), _rows(idx, B), B,
+                                                         dP.data_ptr(), loss.data_ptr()))
+    return dP, loss
+
+
+def mlp_deep_sgd_step(ctx: DeepContext, X, Y, lr, idx=None, B=None, loss=None):
+    n_rows = X.shape[0]
+    B = (n_rows if idx is None else idx.numel()) if B is None else B
+    _dev(X, "X", numel=n_rows * D_IN)
+    _dev(Y, "Y", numel=n_rows)
+    lp = _dev(loss, "loss", numel=1) if loss is not None else None
+    _check("mlp_deep_sgd_step", load().mlp_deep_sgd_step(ctx.handle, X.data_ptr(), n_rows,
+                                                         Y.data_ptr(), _rows(idx, B), B,
+                                                         float(lr), lp))
+    return loss
+
+
+def mlp_deep_train_epochs(ctx: DeepContext, X, Y, batch, lr, epochs, perm=None, max_steps=-1,
+                          epoch_loss=None, step_loss=None):
+    n = X.shape[0]
+    _dev(X, "X", numel=n * D_IN)
+    _dev(Y, "Y", numel=n)
+    pp = _dev(perm, "perm", dtype=torch.int32, numel=epochs * n) if perm is not None else None
+    ep = _dev(epoch_loss, "epoch_loss", numel=epochs) if epoch_loss is not None else None
+    steps = -(-n // batch) * epochs
+    if max_steps >= 0:
+        steps = min(steps, max_steps)
+    sp = _dev(step_loss, "step_loss", numel=steps) if step_loss is not None else None
+    _check("mlp_deep_train_epochs", load().mlp_deep_train_epochs(ctx.handle, X.data_ptr(),
+                                                                 Y.data_ptr(), n, batch, float(lr),
+                                                                 epochs, pp, max_steps, ep, sp))
+
+
+def mlp_deep_check_errors(ctx: DeepContext) -> None:
+    _check("mlp_deep_check_errors", load().mlp_deep_check_errors(ctx.handle))
+
+
+def mlp_deep_profile(ctx: DeepContext, enable: bool) -> None:
+    _check("mlp_deep_profile", load().mlp_deep_profile(ctx.handle, 1 if enable else 0))
+
+
+def mlp_deep_last_kernel_ms(ctx: DeepContext) -> float:
+    ms = _f32(0.0)
+    _check("mlp_deep_last_kernel_ms", load().mlp_deep_last_kernel_ms(ctx.handle, ctypes.byref(ms)))
+    return float(ms.value)

@@ -64,6 +64,26 @@ def test_strategy_workspace_bytes():
     assert lib.mlp_strategy_workspace_bytes(32, 256, 0, 2) == 0
 
 
+def test_deep_sizes_and_checks():
+    lib = _lib()
+    assert lib.mlp_deep_param_count(32, 256, 1) == 8448
+    assert lib.mlp_deep_param_count(32, 256, 3) == 32 * 256 + 2 * 256 * 256 + 256
+    for bad in ((32, 100, 2), (32, 32, 2), (16, 256, 2), (32, 256, 0), (32, 256, 9), (32, 2048, 2)):
+        assert lib.mlp_deep_param_count(*bad) == 0
+        assert lib.mlp_deep_workspace_bytes(*bad, 64) == 0
+    b = lib.mlp_deep_workspace_bytes(32, 256, 3, 4096)
+    assert b >= 4 * (3 * 4096 * 256) and b % 256 == 0
+    assert lib.mlp_deep_workspace_bytes(32, 256, 3, 0) == 0
+    h = ctypes.c_void_p()
+    fake = ctypes.c_void_p(256)
+    assert lib.mlp_deep_init(None, 32, 256, 2, 1, 64, fake, fake, 1 << 30, None) == -1
+    assert lib.mlp_deep_init(ctypes.byref(h), 32, 256, 2, 2, 64, fake, fake, 1 << 30, None) == -2
+    assert lib.mlp_deep_init(ctypes.byref(h), 32, 256, 2, 1, 64, fake, fake, 100, None) == -3
+    assert h.value is None
+    assert lib.mlp_deep_forward(None, fake, 10, None, 10, fake) == -1
+    assert lib.mlp_deep_check_errors(None) == -1
+
+
 def test_status_strings():
     lib = _lib()
     for s in (0, -1, -2, -3, -4, -6):

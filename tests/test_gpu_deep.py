@@ -1,0 +1,231 @@
+"""GPU parity of the L-hidden-layer path (mlp_deep_*) against the deep oracle.
+
+Two kinds of inputs:
+- dyadic: X, Y and every weight are small multiples of 1/4, 1/8 or 1/16, chosen
+  so that every pre-activation is an integer multiple of its scale whose
+  partial sums stay below 2^24 of that scale. Then fp32 computes every Z
+  exactly, in any summation order: the forward must match the oracle bitwise and
+  the ReLU masks cannot differ, so the gradients are held to 1e-5 (only the
+  backward's sums round);
+- Gaussian (the evaluation-workload recipe): the forward and the loss are
+  continuous at the ReLU kink and are held to 1e-5; gradients to 1e-3, since an
+  fp32 pre-activation within rounding of zero may take either mask value
+  (a correct result either way) and deep nets have many of them. At L = 1 the
+  network is the paper's and the gradients meet the main path's 1e-4 bar after
+  the kink alignment of tests/parity.py.
+"""
+import numpy as np
+import pytest
+import torch
+
+import datagen
+import oracle
+from tests.parity import align_kinks, rel
+
+pytestmark = pytest.mark.gpu
+
+D = 32
+
+
+@pytest.fixture(scope="module")
+def mlp():
+    assert torch.cuda.is_available(), "GPU tests need a GPU"
+    from paper_2606_30497_amd import mlp as m
+    m.load(require_built=True)
+    return m
+
+
+def _to(a, dtype=None):
+    t = torch.from_numpy(np.ascontiguousarray(a))
+    if dtype is not None:
+        t = t.to(dtype)
+    return t.cuda()
+
+
+def _gauss_net(rng, h, L):
+    parts = []
+    for l in range(L):
+        K = D if l == 0 else h
+        parts.append(rng.standard_normal(K * h) * np.sqrt(2.0 / K))
+    parts.append(rng.standard_normal(h) * np.sqrt(2.0 / h))
+    return np.concatenate(parts).astype(np.float32)
+
+
+def _dyadic(rng, n, h, L):
+    """Integer numerators with scales 1/4 (X), 1/16 (weights), 1/8 (Y). The
+    forward is run in exact integer arithmetic to check that, for every
+    pre-activation and for Ypred, the sum of the terms' magnitudes (a bound on
+    every partial sum, in units of the entry's scale) stays below 2^24."""
+    Xi = rng.integers(-3, 4, size=(n, D)).astype(np.int64)
+    Wi = [rng.integers(-3, 4, size=(D if l == 0 else h, h)).astype(np.int64) for l in range(L)]
+    woi = rng.integers(-3, 4, size=h).astype(np.int64)
+    Hi = Xi
+    for W in Wi:
+        assert (np.abs(Hi) @ np.abs(W)).max() < 2 ** 24
+        Hi = np.maximum(Hi @ W, 0)
+    assert (Hi @ np.abs(woi)).max() < 2 ** 24
+    X = (Xi / 4.0).astype(np.float32)
+    Y = (rng.integers(-8, 9, size=n) / 8.0).astype(np.float32)
+    P = np.concatenate([W.ravel() / 16.0 for W in Wi] + [woi / 16.0]).astype(np.float32)
+    return X, Y, P
+
+
+def _ctx(mlp, P, h, L, max_batch):
+    p = _to(P.astype(np.float32))
+    return mlp.mlp_deep_init(p, h, L, max_batch), p
+
+
+# --- forward -------------------------------------------------------------------
+
+@pytest.mark.parametrize("h,L", [(64, 1), (64, 2), (64, 3), (128, 2)])
+def test_forward_dyadic_is_exact(mlp, h, L):
+    rng = np.random.default_rng(10 * h + L)
+    X, Y, P = _dyadic(rng, 1000, h, L)
+    ctx, _ = _ctx(mlp, P, h, L, 256)             # 1000 rows: four chunks of max_batch
+    got = mlp.mlp_deep_forward(ctx, _to(X)).cpu().numpy()
+    ref = oracle.deep_forward(X, P, D, h, L)
+    assert np.array_equal(got, ref.astype(np.float32))
+    mlp.mlp_deep_check_errors(ctx)
+
+
+@pytest.mark.parametrize("h,L", [(64, 2), (256, 3), (1024, 2)])
+def test_forward_gaussian(mlp, h, L):
+    rng = np.random.default_rng(h + L)
+    d = datagen.make_data(3001, 32, seed=5, with_perm=False)
+    P = _gauss_net(rng, h, L)
+    ctx, _ = _ctx(mlp, P, h, L, 512)
+    idx = rng.integers(0, 3001, size=1777).astype(np.int32)
+    got = mlp.mlp_deep_forward(ctx, _to(d.X), _to(idx)).cpu().numpy()
+    assert rel(got, oracle.deep_forward(d.X, P, D, h, L, idx=idx)) < 1e-5
+    mlp.mlp_deep_check_errors(ctx)
+
+
+# --- gradients -----------------------------------------------------------------
+
+@pytest.mark.parametrize("h,L", [(64, 1), (64, 2), (64, 3), (128, 3)])
+@pytest.mark.parametrize("B", [1, 16, 64, 256])
+def test_gradients_dyadic(mlp, h, L, B):
+    rng = np.random.default_rng(1000 * L + 7 * h + B)
+    X, Y, P = _dyadic(rng, 600, h, L)
+    ctx, _ = _ctx(mlp, P, h, L, 256)
+    idx = rng.integers(0, 600, size=B).astype(np.int32)
+    dP, loss = mlp.mlp_deep_backward(ctx, _to(X), _to(Y), _to(idx))
+    torch.cuda.synchronize()
+    mlp.mlp_deep_check_errors(ctx)
+    ref, rL, _ = oracle.deep_grad(X, Y, P, D, h, L, idx=idx)
+    assert rel(dP.cpu().numpy(), ref) <= 1e-5
+    assert abs(float(loss.cpu()[0]) - rL) <= 1e-5 * max(rL, 1e-30)
+
+
+@pytest.mark.parametrize("h,L", [(64, 2), (256, 2), (256, 3)])
+@pytest.mark.parametrize("B", [7, 160, 1000])
+def test_gradients_gaussian(mlp, h, L, B):
+    rng = np.random.default_rng(h * L + B)
+    d = datagen.make_data(5000, 32, seed=6, with_perm=False)
+    P = _gauss_net(rng, h, L)
+    ctx, _ = _ctx(mlp, P, h, L, 1024)
+    idx = rng.integers(0, 5000, size=B).astype(np.int32)
+    dP, loss = mlp.mlp_deep_backward(ctx, _to(d.X), _to(d.Y), _to(idx))
+    ref, rL, _ = oracle.deep_grad(d.X, d.Y, P, D, h, L, idx=idx)
+    assert rel(dP.cpu().numpy(), ref) <= 1e-3
+    assert abs(float(loss.cpu()[0]) - rL) <= 1e-5 * rL
+
+
+@pytest.mark.parametrize("h", [64, 256])
+def test_one_layer_meets_the_main_bar(mlp, h):
+    """L = 1 is the paper's network: gradients within 1e-4 of the shallow oracle
+    after the kink alignment used for the main path."""
+    d = datagen.make_data(5000, h, seed=300 + h, with_perm=False)
+    P = np.concatenate([d.W1.ravel(), d.W2]).astype(np.float32)
+    ctx, _ = _ctx(mlp, P, h, 1, 4096)
+    idx = np.random.default_rng(h).integers(0, 5000, size=4096).astype(np.int32)
+    dP, _ = mlp.mlp_deep_backward(ctx, _to(d.X), _to(d.Y), _to(idx))
+    g = dP.cpu().numpy()
+    W1, W2 = d.W1.astype(np.float64), d.W2.astype(np.float64)
+    r1, r2, _, z, zabs = oracle.grad(d.X, d.Y, W1, W2, idx=idx, want_z=True)
+    yp = oracle.forward(d.X, W1, W2, idx=idx)
+    g1 = g[:D * h].reshape(D, h)
+    r1a, _, _ = align_kinks(g1, r1, d.X, d.Y, W1, W2, idx, z, zabs, yp)
+    assert rel(g1, r1a) <= 1e-4
+    assert rel(g[D * h:], r2) <= 1e-4
+
+
+# --- training ------------------------------------------------------------------
+
+def _train(mlp, X, Y, P, h, L, batch, lr, epochs, perm=None, max_steps=-1):
+    ctx, p = _ctx(mlp, P, h, L, batch)
+    n = X.shape[0]
+    steps = -(-n // batch) * epochs if max_steps < 0 else max_steps
+    el = torch.zeros(epochs, dtype=torch.float32, device="cuda")
+    sl = torch.zeros(steps, dtype=torch.float32, device="cuda")
+    mlp.mlp_deep_train_epochs(ctx, _to(X), _to(Y), batch, lr, epochs,
+                              perm=None if perm is None else _to(perm), max_steps=max_steps,
+                              epoch_loss=el, step_loss=sl)
+    torch.cuda.synchronize()
+    mlp.mlp_deep_check_errors(ctx)
+    return p.cpu().numpy(), sl.cpu().numpy(), el.cpu().numpy()
+
+
+@pytest.mark.parametrize("h,L", [(64, 2), (64, 3), (256, 2)])
+def test_train_epochs_with_shuffle_and_tail(mlp, h, L):
+    n, B, E, lr = 1000, 128, 2, 2.0 ** -7                 # tail of 104 rows each epoch
+    rng = np.random.default_rng(h + 10 * L)
+    X, Y, P = _dyadic(rng, n, h, L)
+    perm = np.stack([rng.permutation(n) for _ in range(E)]).astype(np.int32)
+    gP, gsl, gel = _train(mlp, X, Y, P, h, L, B, lr, E, perm=perm)
+    ref = oracle.deep_train(X, Y, P, D, h, L, B, lr, E, perm=perm)
+    assert ref["steps"] == 16 and len(gsl) == 16
+    P0 = P.astype(np.float64)
+    assert rel(gP - P0, ref["P"] - P0) <= 1e-3
+    assert np.all(np.abs(gsl - ref["step_loss"]) <= 1e-3 * ref["step_loss"])
+    assert np.all(np.abs(gel - ref["epoch_loss"]) <= 1e-3 * ref["epoch_loss"])
+
+
+def test_train_gaussian_workload_batch(mlp):
+    """Three SGD steps of a 32-256-256-256-1 net at batch 4096 on the evaluation
+    recipe (He-normal weights, sin target), against the oracle."""
+    h, L, B, lr = 256, 3, 4096, 0.002
+    d = datagen.make_data(20000, 32, epochs=1, seed=1005)
+    P = _gauss_net(np.random.default_rng(7), h, L)
+    gP, gsl, _ = _train(mlp, d.X, d.Y, P, h, L, B, lr, 1, perm=d.perm, max_steps=3)
+    ref = oracle.deep_train(d.X, d.Y, P, D, h, L, B, lr, 1, perm=d.perm, max_steps=3)
+    P0 = P.astype(np.float64)
+    assert rel(gP - P0, ref["P"] - P0) <= 1e-3
+    assert np.all(np.abs(gsl - ref["step_loss"]) <= 1e-4 * ref["step_loss"])
+
+
+def test_deterministic(mlp):
+    rng = np.random.default_rng(3)
+    d = datagen.make_data(3000, 32, epochs=2, seed=8)
+    P = _gauss_net(rng, 128, 3)
+    a = _train(mlp, d.X, d.Y, P, 128, 3, 500, 0.01, 2, perm=d.perm)
+    b = _train(mlp, d.X, d.Y, P, 128, 3, 500, 0.01, 2, perm=d.perm)
+    for x, y in zip(a, b):
+        assert np.array_equal(x, y)
+
+
+# --- errors --------------------------------------------------------------------
+
+def test_errors(mlp):
+    rng = np.random.default_rng(4)
+    P = _gauss_net(rng, 64, 2)
+    ctx, p = _ctx(mlp, P, 64, 2, 64)
+    X = _to(rng.standard_normal((100, D)).astype(np.float32))
+    Y = _to(rng.standard_normal(100).astype(np.float32))
+    idx = np.arange(64, dtype=np.int32)
+    idx[9] = 100                                      # one past the end: read as row 0, flagged
+    mlp.mlp_deep_backward(ctx, X, Y, _to(idx))
+    with pytest.raises(mlp.MLPError) as ei:
+        mlp.mlp_deep_check_errors(ctx)
+    assert ei.value.status == -6
+    mlp.mlp_deep_check_errors(ctx)
+    lib = mlp.load()
+    before = p.clone()
+    assert lib.mlp_deep_sgd_step(ctx.handle, X.data_ptr(), 100, Y.data_ptr(), None, 65,
+                                 0.1, None) == -1           # B > max_batch
+    assert lib.mlp_deep_sgd_step(ctx.handle, X.data_ptr(), 100, Y.data_ptr(), None, 10,
+                                 float("nan"), None) == -1
+    assert lib.mlp_deep_train_epochs(ctx.handle, X.data_ptr(), Y.data_ptr(), 100, 0, 0.1, 1,
+                                     None, -1, None, None) == -1
+    torch.cuda.synchronize()
+    assert torch.equal(before, p)
