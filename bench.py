@@ -204,7 +204,18 @@ def measure_forward(h, X, args, mlp, torch, np):
     ms = float(np.mean([e0.elapsed_time(e1) for e0, e1 in ev]))
     flop = 66.0 * h * n
     achieved = flop / (ms / 1e3) / 1e12
-    return {
+    extra = {}
+    if not args.no_cpu_baseline:
+        import oracle
+        Xh = X.cpu().numpy() if n <= 200_000 else X[:200_000].cpu().numpy()
+        rows = max(1000, min(Xh.shape[0], int(2e9 / (66.0 * h))))   # about 2 GFLOP of fp64 work
+        t = time.perf_counter()
+        oracle.forward(Xh[:rows], d.W1, d.W2)
+        dt = time.perf_counter() - t
+        extra["cpu_baseline"] = {"value": rows / dt, "unit": "rows/s", "cores": 1, "kind": "oracle",
+                                 "sample": "oracle forward over the first %d rows, fp64, one thread"
+                                           % rows}
+    return dict({
         "metric": "forward rows/sec (eqs. 11-13 over a resident dataset)",
         "value": n / ((t1 - t0) / args.steps),
         "unit": "rows/s",
@@ -221,7 +232,7 @@ def measure_forward(h, X, args, mlp, torch, np):
                      "kernel_ms": ms, "flop_per_launch": flop,
                      "hbm_gbs": 132.0 * n / (ms / 1e3) / 1e9,
                      "hbm_frac": 132.0 * n / (ms / 1e3) / 1e9 / HBM_PEAK_GBS},
-    }
+    }, **extra)
 
 
 def measure_deep(w, args, mlp, torch, np):
