@@ -27,9 +27,9 @@
 //
 // GEMM tile: 64 x 64 outputs per workgroup of four waves (each 32 x 32, 2 x 2
 // v_mfma_f32_16x16x4f32 tiles), K in chunks of 32 staged in LDS k-major with a
-// row stride of 80 floats, so that the 16 lanes reading one MFMA operand row
-// and the next k row fall in different banks; the next chunk's global loads
-// are in flight while the current chunk is computed.
+// row stride of 80 floats (k-major) or 34 (m-major), so that MFMA operand reads
+// are conflict-free; the next two chunks' global loads are in flight while the
+// current chunk is computed.
 #include <hip/hip_runtime.h>
 
 #include <math.h>
@@ -60,31 +60,47 @@ struct Stage {
     float4 a[2], b[2];
 };
 
+// Loads are unconditional, from an address clamped into the operand, and the
+// value is replaced by zero where the element lies outside it: a load under a
+// lane condition would compile to a branch followed by a wait for that load,
+// serialising the chunk's loads.
+// v where ok, zeros elsewhere, component by component (a select of the whole
+// struct can be lowered through a stack slot)
+__device__ __forceinline__ float4 keep_if(bool ok, float4 v) {
+    return make_float4(ok ? v.x : 0.f, ok ? v.y : 0.f, ok ? v.z : 0.f, ok ? v.w : 0.f);
+}
+
 template <int OP>
 __device__ __forceinline__ void gemm_fetch(Stage &st, const float *__restrict__ A, int lda,
                                            const float *__restrict__ B, int ldb, int64_t M, int N,
                                            int64_t m0, int n0, int64_t k0, int64_t ke, int t) {
-    const float4 z = make_float4(0.f, 0.f, 0.f, 0.f);
 #pragma unroll
     for (int h = 0; h < 2; ++h) {
         if constexpr (OP == OP_TN) {              // a(m, k) = A[k lda + m]: float4 along m
-            const int kk = (t >> 4) + 16 * h, mq = (t & 15) * 4;
-            st.a[h] = (k0 + kk < ke && m0 + mq < M)
-                          ? *reinterpret_cast<const float4 *>(A + (k0 + kk) * lda + m0 + mq) : z;
+            const int64_t k = k0 + (t >> 4) + 16 * h, m = m0 + (t & 15) * 4;
+            const bool ok = k < ke && m < M;
+            const float4 v = *reinterpret_cast<const float4 *>(
+                A + (k < ke ? k : ke - 1) * lda + (m < M ? m : M - 4));
+            st.a[h] = keep_if(ok, v);
         } else {                                  // a(m, k) = A[m lda + k]: float4 along k
-            const int row = t >> 2, kq = (t & 3) * 4 + 16 * h;
-            st.a[h] = (m0 + row < M && k0 + kq < ke)
-                          ? *reinterpret_cast<const float4 *>(A + (m0 + row) * lda + k0 + kq) : z;
+            const int64_t m = m0 + (t >> 2), k = k0 + (t & 3) * 4 + 16 * h;
+            const bool ok = m < M && k < ke;
+            const float4 v = *reinterpret_cast<const float4 *>(
+                A + (m < M ? m : M - 1) * lda + (k < ke ? k : ke - 4));
+            st.a[h] = keep_if(ok, v);
         }
         if constexpr (OP == OP_NT) {              // b(k, n) = B[n ldb + k]: float4 along k
-            const int col = t >> 2, kq = (t & 3) * 4 + 16 * h;
-            st.b[h] = (n0 + col < N && k0 + kq < ke)
-                          ? *reinterpret_cast<const float4 *>(B + (int64_t)(n0 + col) * ldb + k0 + kq)
-                          : z;
+            const int64_t n = n0 + (t >> 2), k = k0 + (t & 3) * 4 + 16 * h;
+            const bool ok = n < N && k < ke;
+            const float4 v = *reinterpret_cast<const float4 *>(
+                B + (n < N ? n : N - 1) * ldb + (k < ke ? k : ke - 4));
+            st.b[h] = keep_if(ok, v);
         } else {                                  // b(k, n) = B[k ldb + n]: float4 along n
-            const int kk = (t >> 4) + 16 * h, nq = (t & 15) * 4;
-            st.b[h] = (k0 + kk < ke && n0 + nq < N)
-                          ? *reinterpret_cast<const float4 *>(B + (k0 + kk) * ldb + n0 + nq) : z;
+            const int64_t k = k0 + (t >> 4) + 16 * h, n = n0 + (t & 15) * 4;
+            const bool ok = k < ke && n < N;
+            const float4 v = *reinterpret_cast<const float4 *>(
+                B + (k < ke ? k : ke - 1) * ldb + (n < N ? n : N - 4));
+            st.b[h] = keep_if(ok, v);
         }
     }
 }
@@ -121,7 +137,8 @@ __device__ __forceinline__ void gemm_stash(const Stage &st, float *As, float *Bs
 // Grid: (ceil(M/64), ceil(N/64), splits); split z covers k in [z kc, min(K, z kc + kc))
 // and writes C + z * c_split. N and the contiguous dimension of every operand
 // are multiples of 16 (hidden widths and d_in); M and K are arbitrary. The next
-// K chunk is loaded into registers while the current one is on the matrix cores.
+// two K chunks are loaded into registers while the current one is on the matrix
+// cores.
 template <int OP, int EP>
 __global__ __launch_bounds__(256) void k_gemm(const float *__restrict__ A, int lda,
                                               const float *__restrict__ B, int ldb,
@@ -145,12 +162,15 @@ __global__ __launch_bounds__(256) void k_gemm(const float *__restrict__ A, int l
 #pragma unroll
         for (int j = 0; j < 2; ++j) acc[i][j] = f4{0.f, 0.f, 0.f, 0.f};
 
-    Stage st;
-    gemm_fetch<OP>(st, A, lda, B, ldb, M, N, m0, n0, kb, ke, t);
-    for (int64_t k0 = kb; k0 < ke; k0 += GK) {
-        gemm_stash<OP>(st, As, Bs, t);
+    // two chunks in flight: chunk c + 2 is fetched into the registers chunk c
+    // has just left, while chunk c is on the matrix cores
+    Stage s0, s1;
+    gemm_fetch<OP>(s0, A, lda, B, ldb, M, N, m0, n0, kb, ke, t);
+    if (kb + GK < ke) gemm_fetch<OP>(s1, A, lda, B, ldb, M, N, m0, n0, kb + GK, ke, t);
+    auto chunk = [&](Stage &cur, int64_t kp) __attribute__((always_inline)) {
+        gemm_stash<OP>(cur, As, Bs, t);
         __syncthreads();
-        if (k0 + GK < ke) gemm_fetch<OP>(st, A, lda, B, ldb, M, N, m0, n0, k0 + GK, ke, t);
+        if (kp + 2 * GK < ke) gemm_fetch<OP>(cur, A, lda, B, ldb, M, N, m0, n0, kp + 2 * GK, ke, t);
         // eight k steps of 4 on the matrix cores
 #pragma unroll
         for (int ks = 0; ks < GK / 4; ++ks) {
@@ -173,6 +193,10 @@ __global__ __launch_bounds__(256) void k_gemm(const float *__restrict__ A, int l
                     acc[i][j] = __builtin_amdgcn_mfma_f32_16x16x4f32(a[i], b[j], acc[i][j], 0, 0, 0);
         }
         __syncthreads();
+    };
+    for (int64_t k0 = kb; k0 < ke; k0 += 2 * GK) {
+        chunk(s0, k0);
+        if (k0 + GK < ke) chunk(s1, k0 + GK);
     }
     // ---- epilogue: lane holds C[4 lq + v][li] of each 16 x 16 tile ----
     float *Cz = C + (int64_t)blockIdx.z * c_split;
