@@ -17,11 +17,11 @@
 //   k_gemm<TN, NONE>   dW_l = H_{l-1}^T G_l, split over row chunks (grid z);
 //                      each chunk writes its own partial, summed in chunk order
 //   k_gemm<NT, MASK>   G_{l-1} = (G_l W_l^T) masked by H_{l-1} > 0
-//   k_deep_out         Ypred, residual, dZ_o and G_L, one wave per row
-//   k_deep_dwo         dw_o partials per row chunk
-//   k_deep_loss        the batch loss, one workgroup, fixed tree
+//   k_deep_out         Ypred, residual, dZ_o, G_L and the dw_o partial of a
+//                      chunk of rows (one wave per row)
 //   k_deep_apply       sums every gradient's chunk partials in order and
-//                      applies eq. 19 (or writes the gradients)
+//                      applies eq. 19 (or writes the gradients); its last
+//                      workgroup reduces the batch loss in a fixed tree
 // Every output element is one lane's sum in a fixed order, so results are
 // bitwise reproducible.
 //
@@ -48,7 +48,8 @@ constexpr int GK = 32;        // K chunk
 constexpr int GLS = 80;       // LDS row stride of a k-major operand tile ([k][m], floats)
 constexpr int GMS = 34;       // LDS row stride of an m-major operand tile ([m][k], floats)
 constexpr int GLDS = GK * GLS;   // floats per operand tile (>= GT * GMS)
-constexpr int SPLIT_MAX = 16; // row chunks of the weight-gradient products
+constexpr int SPLIT_MAX = 64; // row chunks of a weight-gradient product
+constexpr int OUT_CHUNKS_MAX = 256;   // row chunks of the output layer (dw_o partials)
 constexpr int DEEP_MAX_LAYERS = 8;
 
 enum { OP_NN = 0, OP_TN = 1, OP_NT = 2 };
@@ -238,15 +239,10 @@ __global__ __launch_bounds__(256) void k_deep_gather(const float *__restrict__ X
     if (q == 0) Yb[t] = Y ? Y[r] : 0.0f;
 }
 
-// One wave per row: Ypred = H_L w_o (eq. 13); for training also the residual,
-// dZ_o = (2/n_b) r (eq. 15), r^2, and G_L = dZ_o w_o^T (.) [H_L > 0] (eq. 17).
-template <bool TRAIN>
-__global__ __launch_bounds__(256) void k_deep_out(const float *__restrict__ H, int h,
-                                                  const float *__restrict__ wo,
-                                                  const float *__restrict__ Yb, int64_t nb,
-                                                  float scale, float *__restrict__ ypred,
-                                                  float *__restrict__ dz, float *__restrict__ sq,
-                                                  float *__restrict__ Gout) {
+// Forward output, one wave per row: Ypred = H_L w_o (eq. 13).
+__global__ __launch_bounds__(256) void k_deep_ypred(const float *__restrict__ H, int h,
+                                                    const float *__restrict__ wo, int64_t nb,
+                                                    float *__restrict__ ypred) {
     const int lane = threadIdx.x & 63;
     const int64_t r = (int64_t)blockIdx.x * 4 + (threadIdx.x >> 6);
     if (r >= nb) return;
@@ -254,95 +250,116 @@ __global__ __launch_bounds__(256) void k_deep_out(const float *__restrict__ H, i
     float s = 0.0f;
     for (int j = lane; j < h; j += 64) s = fmaf(hr[j], wo[j], s);
     s = sum64(s);
-    if (!TRAIN) {
-        if (lane == 0) ypred[r] = s;
-        return;
-    }
-    const float res = s - Yb[r];
-    const float g = scale * res;
-    if (lane == 0) {
-        dz[r] = g;
-        sq[r] = res * res;
-    }
-    float *gr = Gout + r * h;
-    for (int j = lane; j < h; j += 64) gr[j] = hr[j] > 0.0f ? g * wo[j] : 0.0f;
+    if (lane == 0) ypred[r] = s;
 }
 
-// dw_o partial of row chunk z (eq. 16): part[z][j] = sum over the chunk's rows
-// of H_L[r][j] dZ_o[r]. A workgroup covers 16 units with 16 row phases (thread
-// (p, u): unit 16 bx + u, rows rb + p, rb + p + 16, ... ascending); the 16
-// phase sums meet in LDS and are added in phase order.
-__global__ __launch_bounds__(256) void k_deep_dwo(const float *__restrict__ H, int h,
-                                                  const float *__restrict__ dz, int64_t nb,
-                                                  int64_t kc, float *__restrict__ part,
-                                                  int64_t p_split) {
-    __shared__ float ps[16][17];
-    const int u = threadIdx.x & 15, ph = threadIdx.x >> 4;
-    const int j = blockIdx.x * 16 + u;
-    const int64_t rb = (int64_t)blockIdx.y * kc;
+// Output layer of a training step over row chunk z = blockIdx.x (rows [z kc,
+// min(nb, z kc + kc))); wave w takes rows w, w + 4, ... of the chunk and lane l
+// units l, l + 64, ... (HU of them). Per row: Ypred = H_L w_o (eq. 13),
+// r = Ypred - Y, r^2, dZ_o = (2/n_b) r (eq. 15) and G_L = dZ_o w_o^T (.)
+// [H_L > 0] (eq. 17); each lane also sums H_L[r][j] dZ_o[r] over its rows
+// (eq. 16), and the four waves' sums are added in wave order into the chunk's
+// dw_o partial.
+template <int HU>
+__global__ __launch_bounds__(256) void k_deep_out(const float *__restrict__ H, int h,
+                                                  const float *__restrict__ wo,
+                                                  const float *__restrict__ Yb, int64_t nb,
+                                                  int64_t kc, float scale, float *__restrict__ sq,
+                                                  float *__restrict__ Gout,
+                                                  float *__restrict__ dwo_part) {
+    __shared__ float wsum[4][64 * HU];
+    const int lane = threadIdx.x & 63, wave = threadIdx.x >> 6;
+    const int64_t rb = (int64_t)blockIdx.x * kc;
     const int64_t re = rb + kc < nb ? rb + kc : nb;
-    float s = 0.0f;
-    if (j < h)
-        for (int64_t r = rb + ph; r < re; r += 16) s = fmaf(H[r * h + j], dz[r], s);
-    ps[ph][u] = s;
-    __syncthreads();
-    if (ph == 0 && j < h) {
-        float tot = 0.0f;
+    float wov[HU], acc[HU];
 #pragma unroll
-        for (int q = 0; q < 16; ++q) tot += ps[q][u];
-        part[(int64_t)blockIdx.y * p_split + j] = tot;
+    for (int i = 0; i < HU; ++i) {
+        wov[i] = wo[lane + 64 * i];
+        acc[i] = 0.0f;
     }
-}
-
-// Batch loss (eq. 14): one workgroup, thread i sums rows i, i + 256, ... then a
-// fixed binary tree; step and epoch loss as in the one-layer paths.
-__global__ __launch_bounds__(256) void k_deep_loss(const float *__restrict__ sq, int64_t nb,
-                                                   ReduceArgs a) {
-    __shared__ float part[256];
-    const int i = threadIdx.x;
-    float s = 0.0f;
-    for (int64_t t = i; t < nb; t += 256) s += sq[t];
-    part[i] = s;
-    __syncthreads();
-    for (int w = 128; w >= 1; w >>= 1) {
-        if (i < w) part[i] += part[i + w];
-        __syncthreads();
-    }
-    if (i == 0) {
-        const float sse = part[0];
-        const float L = sse * a.inv_nb;
-        if (a.loss) a.loss[0] = L;
-        if (a.step_loss) a.step_loss[a.step] = L;
-        if (a.epoch_loss) {
-            double acc = a.first_in_epoch ? 0.0 : a.ctl->epoch_sse;
-            acc += (double)sse;
-            a.ctl->epoch_sse = acc;
-            a.epoch_loss[a.epoch] = (float)(acc * a.inv_n);
+    for (int64_t r = rb + wave; r < re; r += 4) {
+        const float *hr = H + r * h;
+        float hv[HU];
+        float s = 0.0f;
+#pragma unroll
+        for (int i = 0; i < HU; ++i) {
+            hv[i] = hr[lane + 64 * i];
+            s = fmaf(hv[i], wov[i], s);
+        }
+        s = sum64(s);
+        const float res = s - Yb[r];
+        const float g = scale * res;
+        if (lane == 0) sq[r] = res * res;
+        float *gr = Gout + r * h;
+#pragma unroll
+        for (int i = 0; i < HU; ++i) {
+            gr[lane + 64 * i] = hv[i] > 0.0f ? g * wov[i] : 0.0f;
+            acc[i] = fmaf(hv[i], g, acc[i]);
         }
     }
+#pragma unroll
+    for (int i = 0; i < HU; ++i) wsum[wave][lane + 64 * i] = acc[i];
+    __syncthreads();
+    for (int j = threadIdx.x; j < h; j += 256)
+        dwo_part[(int64_t)blockIdx.x * h + j] = ((wsum[0][j] + wsum[1][j]) + wsum[2][j]) + wsum[3][j];
 }
 
 // Row-chunk split of each parameter segment's gradient (W_1 .. W_L, then w_o).
+// Segment s keeps its chunk partials at part + part_off[s], chunk z at
+// z * size(s).
 struct SplitPlan {
     int nseg;
     int64_t seg_end[DEEP_MAX_LAYERS + 1];   // exclusive end of segment s in the flat array
     int splits[DEEP_MAX_LAYERS + 1];        // row chunks (partials) of segment s
     int64_t kc[DEEP_MAX_LAYERS + 1];        // rows per chunk
+    int64_t part_off[DEEP_MAX_LAYERS + 1];  // offset of segment s's partials
 };
 
 // Sum the chunk partials of every parameter's gradient in chunk order, then
-// eq. 19 (sgd) or write the gradient.
+// eq. 19 (sgd) or write the gradient. The last workgroup reduces the batch loss
+// instead (eq. 14): thread i sums rows i, i + 256, ..., then a fixed binary
+// tree; step and epoch loss as in the one-layer paths.
 __global__ __launch_bounds__(256) void k_deep_apply(const float *__restrict__ part, SplitPlan sp,
                                                     int64_t np, float *__restrict__ params,
-                                                    float *__restrict__ dparams, float lr, int sgd) {
+                                                    float *__restrict__ dparams, float lr, int sgd,
+                                                    const float *__restrict__ sq, int64_t nb,
+                                                    ReduceArgs ra) {
+    if (blockIdx.x == gridDim.x - 1) {
+        __shared__ float red[256];
+        const int i = threadIdx.x;
+        float v = 0.0f;
+        for (int64_t t = i; t < nb; t += 256) v += sq[t];
+        red[i] = v;
+        __syncthreads();
+        for (int w = 128; w >= 1; w >>= 1) {
+            if (i < w) red[i] += red[i + w];
+            __syncthreads();
+        }
+        if (i == 0) {
+            const float sse = red[0];
+            const float L = sse * ra.inv_nb;
+            if (ra.loss) ra.loss[0] = L;
+            if (ra.step_loss) ra.step_loss[ra.step] = L;
+            if (ra.epoch_loss) {
+                double acc = ra.first_in_epoch ? 0.0 : ra.ctl->epoch_sse;
+                acc += (double)sse;
+                ra.ctl->epoch_sse = acc;
+                ra.epoch_loss[ra.epoch] = (float)(acc * ra.inv_n);
+            }
+        }
+        return;
+    }
     const int64_t p = (int64_t)blockIdx.x * 256 + threadIdx.x;
     if (p >= np) return;
     int seg = 0;
     while (seg + 1 < sp.nseg && p >= sp.seg_end[seg]) ++seg;
-    float s = 0.0f;
-    for (int z = 0; z < sp.splits[seg]; ++z) s += part[(int64_t)z * np + p];
-    if (sgd) params[p] -= lr * s;
-    else dparams[p] = s;
+    const int64_t start = seg == 0 ? 0 : sp.seg_end[seg - 1];
+    const int64_t size = sp.seg_end[seg] - start;
+    const float *q = part + sp.part_off[seg] + (p - start);
+    float v = 0.0f;
+    for (int z = 0; z < sp.splits[seg]; ++z) v += q[(int64_t)z * size];
+    if (sgd) params[p] -= lr * v;
+    else dparams[p] = v;
 }
 
 // ---------------------------------------------------------------------------
@@ -354,10 +371,11 @@ struct DeepCtx {
     int64_t max_batch = 0, np = 0;
     float *params = nullptr;
     Control *ctl = nullptr;
-    float *Xb = nullptr, *Yb = nullptr, *dz = nullptr, *sq = nullptr, *yp = nullptr;
+    float *Xb = nullptr, *Yb = nullptr, *sq = nullptr;
     float *H = nullptr;       // [layers][max_batch x hidden]
     float *G[2] = {nullptr, nullptr};
-    float *part = nullptr;    // [SPLIT_MAX][np]
+    float *part = nullptr;    // gradient partials, segment s at part_off[s] (plan of max_batch)
+    int64_t part_off[DEEP_MAX_LAYERS + 1] = {};
     hipStream_t stream = nullptr;
     bool profile = false, ev_valid = false;
     hipEvent_t ev0 = nullptr, ev1 = nullptr;
@@ -374,31 +392,61 @@ static bool deep_shape_ok(int32_t d_in, int32_t hidden, int32_t layers) {
            layers <= DEEP_MAX_LAYERS;
 }
 
-static size_t deep_ws_floats(int h, int L, int64_t mb) {
-    const size_t b = (size_t)mb;
-    return pad64f(CTL_BYTES / 4) + pad64f(b * D_IN) + 4 * pad64f(b) +
-           (size_t)(L + 2) * pad64f(b * (size_t)h) + (size_t)SPLIT_MAX * pad64f((size_t)deep_np(h, L));
+// Row chunks of segment s's gradient before rounding the chunk length: a weight
+// segment W_l gets enough chunks for its GEMM to reach about 512 workgroups
+// (output tiles x chunks), at most SPLIT_MAX, with at least 64 rows a chunk; w_o
+// gets one chunk per 64 rows of the output kernel, at most OUT_CHUNKS_MAX. This
+// count never falls as nb grows, and the chunks a plan uses never exceed it, so
+// the count at max_batch sizes the partial buffer for every batch.
+static int64_t seg_chunks(int h, int L, int64_t nb, int s) {
+    int64_t splits;
+    if (s < L) {
+        const int64_t K = s == 0 ? D_IN : h;
+        const int64_t tiles = ((K + GT - 1) / GT) * (h / GT);
+        splits = (512 + tiles - 1) / tiles;
+        const int64_t by_rows = (nb + 63) / 64;
+        if (splits > by_rows) splits = by_rows;
+        splits = splits > SPLIT_MAX ? SPLIT_MAX : splits;
+    } else {
+        splits = (nb + 63) / 64;
+        splits = splits > OUT_CHUNKS_MAX ? OUT_CHUNKS_MAX : splits;
+    }
+    return splits < 1 ? 1 : splits;
 }
 
-// Row chunks of the weight-gradient products for a batch of nb rows: enough
-// chunks that a segment's workgroups (output tiles x chunks) reach about 512,
-// at most SPLIT_MAX, and at least 64 rows per chunk.
-static void split_plan(int h, int L, int64_t nb, SplitPlan *sp) {
+static int64_t seg_size(int h, int L, int s) { return s < L ? (s == 0 ? D_IN : h) * (int64_t)h : h; }
+
+// Offsets of each segment's partials for batches up to mb (packed).
+static int64_t part_layout(int h, int L, int64_t mb, int64_t *off) {
+    int64_t o = 0;
+    for (int s = 0; s <= L; ++s) {
+        if (off) off[s] = o;
+        o += pad64f((size_t)(seg_chunks(h, L, mb, s) * seg_size(h, L, s)));
+    }
+    return o;
+}
+
+// The plan of a batch of nb rows: chunk length rounded up to the GEMM's K chunk,
+// and the chunk count that length gives (never more than seg_chunks).
+static void split_plan(int h, int L, int64_t nb, const int64_t *part_off, SplitPlan *sp) {
     sp->nseg = L + 1;
     for (int s = 0; s <= L; ++s) {
-        // segment s < L: W_{s+1}, tiles of 64 x 64 over [K x h]; s = L: w_o, 16 units a workgroup
-        const int64_t K = s == 0 ? D_IN : h;
-        const int64_t tiles = s < L ? ((K + GT - 1) / GT) * (h / GT) : h / 16;
-        int splits = (int)((512 + tiles - 1) / tiles);
-        const int64_t by_rows = (nb + 63) / 64;
-        if (splits > by_rows) splits = (int)by_rows;
-        splits = splits < 1 ? 1 : (splits > SPLIT_MAX ? SPLIT_MAX : splits);
+        const int64_t splits = seg_chunks(h, L, nb, s);
         int64_t c = (nb + splits - 1) / splits;
         c = (c + GK - 1) / GK * GK;
         sp->kc[s] = c;
         sp->splits[s] = (int)((nb + c - 1) / c);
         sp->seg_end[s] = s < L ? layer_offset(h, s + 2) : deep_np(h, L);
+        sp->part_off[s] = part_off[s];
     }
+}
+
+static int64_t part_floats(int h, int L, int64_t nb) { return part_layout(h, L, nb, nullptr); }
+
+static size_t deep_ws_floats(int h, int L, int64_t mb) {
+    const size_t b = (size_t)mb;
+    return pad64f(CTL_BYTES / 4) + pad64f(b * D_IN) + 2 * pad64f(b) +
+           (size_t)(L + 2) * pad64f(b * (size_t)h) + (size_t)part_floats(h, L, mb);
 }
 
 template <int OP, int EP>
@@ -434,6 +482,25 @@ static hipError_t deep_forward_layers(const DeepCtx &c, int64_t nb) {
     return hipSuccess;
 }
 
+// The training output kernel, instantiated for h / 64 units per lane.
+static hipError_t launch_out(const DeepCtx &c, const float *HL, const float *wo, int64_t nb,
+                             int64_t kc, int chunks, float *dwo_part) {
+    const float scale = 2.0f / (float)nb;   // eq. 15
+    switch (c.hidden / 64) {
+#define DEEP_OUT_CASE(U)                                                                          \
+    case U:                                                                                       \
+        hipLaunchKernelGGL((k_deep_out<U>), dim3(chunks), dim3(256), 0, c.stream, HL, c.hidden, wo, \
+                           c.Yb, nb, kc, scale, c.sq, c.G[0], dwo_part);                           \
+        return hipGetLastError();
+        DEEP_OUT_CASE(1) DEEP_OUT_CASE(2) DEEP_OUT_CASE(3) DEEP_OUT_CASE(4)
+        DEEP_OUT_CASE(5) DEEP_OUT_CASE(6) DEEP_OUT_CASE(7) DEEP_OUT_CASE(8)
+        DEEP_OUT_CASE(9) DEEP_OUT_CASE(10) DEEP_OUT_CASE(11) DEEP_OUT_CASE(12)
+        DEEP_OUT_CASE(13) DEEP_OUT_CASE(14) DEEP_OUT_CASE(15) DEEP_OUT_CASE(16)
+#undef DEEP_OUT_CASE
+    }
+    return hipErrorInvalidValue;
+}
+
 // One step (or one gradient evaluation) on batch rows [off, off + nb) of idx.
 static hipError_t deep_step(DeepCtx &c, const float *X, int64_t n_rows, const float *Y,
                             const int32_t *idx, int64_t off, int64_t nb, const ReduceArgs &ra,
@@ -447,22 +514,16 @@ static hipError_t deep_step(DeepCtx &c, const float *X, int64_t n_rows, const fl
     const float *HL = c.H + (int64_t)(L - 1) * mbh;
     const float *wo = c.params + layer_offset(h, L + 1);
     int cur = 0;
-    hipLaunchKernelGGL((k_deep_out<true>), dim3(blocks_of(nb, 4)), dim3(256), 0, c.stream, HL, h, wo,
-                       c.Yb, nb, 2.0f / (float)nb, nullptr, c.dz, c.sq, c.G[cur]);
-    DEEP_TRY(hipGetLastError());
-    hipLaunchKernelGGL(k_deep_loss, dim3(1), dim3(256), 0, c.stream, c.sq, nb, ra);
-    DEEP_TRY(hipGetLastError());
     SplitPlan sp;
-    split_plan(h, L, nb, &sp);
-    hipLaunchKernelGGL(k_deep_dwo, dim3(blocks_of(h, 16), sp.splits[L]), dim3(256), 0, c.stream, HL,
-                       h, c.dz, nb, sp.kc[L], c.part + layer_offset(h, L + 1), c.np);
-    DEEP_TRY(hipGetLastError());
+    split_plan(h, L, nb, c.part_off, &sp);
+    // output layer: r^2, G_L and the dw_o partials of each row chunk
+    DEEP_TRY(launch_out(c, HL, wo, nb, sp.kc[L], sp.splits[L], c.part + sp.part_off[L]));
     for (int l = L; l >= 1; --l) {
         const int K = l == 1 ? D_IN : h;
         const float *Hin = l == 1 ? c.Xb : c.H + (int64_t)(l - 2) * mbh;
         // dW_l = H_{l-1}^T G_l, eq. 18, split over row chunks
-        DEEP_TRY((gemm<OP_TN, EP_NONE>(c.stream, Hin, K, c.G[cur], h, c.part + layer_offset(h, l), h,
-                                       c.np, K, h, nb, sp.splits[l - 1], sp.kc[l - 1])));
+        DEEP_TRY((gemm<OP_TN, EP_NONE>(c.stream, Hin, K, c.G[cur], h, c.part + sp.part_off[l - 1], h,
+                                       (int64_t)K * h, K, h, nb, sp.splits[l - 1], sp.kc[l - 1])));
         if (l > 1) {
             // G_{l-1} = (G_l W_l^T) (.) [H_{l-1} > 0], eq. 17 one layer down
             DEEP_TRY((gemm<OP_NT, EP_MASK>(c.stream, c.G[cur], h, c.params + layer_offset(h, l), h,
@@ -470,8 +531,9 @@ static hipError_t deep_step(DeepCtx &c, const float *X, int64_t n_rows, const fl
             cur ^= 1;
         }
     }
-    hipLaunchKernelGGL(k_deep_apply, dim3(blocks_of(c.np, 256)), dim3(256), 0, c.stream, c.part,
-                       sp, c.np, c.params, dparams, ra.lr, ra.sgd);
+    // every gradient's partials summed and applied; the last workgroup takes the loss
+    hipLaunchKernelGGL(k_deep_apply, dim3(blocks_of(c.np, 256) + 1), dim3(256), 0, c.stream, c.part,
+                       sp, c.np, c.params, dparams, ra.lr, ra.sgd, c.sq, nb, ra);
     return hipGetLastError();
 }
 
@@ -519,14 +581,12 @@ extern "C" mlp_status mlp_deep_init(mlp_deep_t *out, int32_t d_in, int32_t hidde
     c->ctl = (Control *)take(CTL_BYTES / 4);
     c->Xb = take(b * D_IN);
     c->Yb = take(b);
-    c->dz = take(b);
     c->sq = take(b);
-    c->yp = take(b);
     c->H = p;
     p += (size_t)layers * pad64f(bh);
     c->G[0] = take(bh);
     c->G[1] = take(bh);
-    c->part = take((size_t)SPLIT_MAX * (size_t)c->np);
+    c->part = take((size_t)part_layout(hidden, layers, max_batch, c->part_off));
     Ctx tmp;
     tmp.ctl = c->ctl;
     tmp.stream = c->stream;
@@ -560,8 +620,8 @@ extern "C" mlp_status mlp_deep_forward(mlp_deep_t c, const float *X, int64_t n_r
                            c->stream, X, nullptr, n_rows, idx, off, nb, c->Xb, c->Yb, &c->ctl->err);
         if (hipGetLastError() != hipSuccess) return MLP_ERR_HIP;
         if (deep_forward_layers(*c, nb) != hipSuccess) return MLP_ERR_HIP;
-        hipLaunchKernelGGL((k_deep_out<false>), dim3(blocks_of(nb, 4)), dim3(256), 0, c->stream, HL,
-                           h, wo, nullptr, nb, 0.0f, Ypred + off, nullptr, nullptr, nullptr);
+        hipLaunchKernelGGL(k_deep_ypred, dim3(blocks_of(nb, 4)), dim3(256), 0, c->stream, HL, h, wo,
+                           nb, Ypred + off);
         if (hipGetLastError() != hipSuccess) return MLP_ERR_HIP;
     }
     return MLP_OK;
