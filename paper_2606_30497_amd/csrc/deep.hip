@@ -257,9 +257,11 @@ __global__ __launch_bounds__(256) void k_deep_ypred(const float *__restrict__ H,
 // min(nb, z kc + kc))); wave w takes rows w, w + 4, ... of the chunk and lane l
 // units l, l + 64, ... (HU of them). Per row: Ypred = H_L w_o (eq. 13),
 // r = Ypred - Y, r^2, dZ_o = (2/n_b) r (eq. 15) and G_L = dZ_o w_o^T (.)
-// [H_L > 0] (eq. 17); each lane also sums H_L[r][j] dZ_o[r] over its rows
-// (eq. 16), and the four waves' sums are added in wave order into the chunk's
-// dw_o partial.
+// [H_L > 0] (eq. 17); each lane also sums H_L[r][j] dZ_o[r] over its rows in
+// row order (eq. 16), and the four waves' sums are added in wave order into
+// the chunk's dw_o partial. A wave loads OUT_R rows before it reduces any of
+// them, so that their loads are in flight together.
+constexpr int OUT_R = 4;
 template <int HU>
 __global__ __launch_bounds__(256) void k_deep_out(const float *__restrict__ H, int h,
                                                   const float *__restrict__ wo,
@@ -277,24 +279,34 @@ __global__ __launch_bounds__(256) void k_deep_out(const float *__restrict__ H, i
         wov[i] = wo[lane + 64 * i];
         acc[i] = 0.0f;
     }
-    for (int64_t r = rb + wave; r < re; r += 4) {
-        const float *hr = H + r * h;
-        float hv[HU];
-        float s = 0.0f;
+    for (int64_t r0 = rb + wave; r0 < re; r0 += 4 * OUT_R) {
+        // rows past the chunk load its last row and are dropped below
+        float hv[OUT_R][HU], yv[OUT_R];
 #pragma unroll
-        for (int i = 0; i < HU; ++i) {
-            hv[i] = hr[lane + 64 * i];
-            s = fmaf(hv[i], wov[i], s);
+        for (int j = 0; j < OUT_R; ++j) {
+            const int64_t r = r0 + 4 * j < re ? r0 + 4 * j : re - 1;
+            const float *hr = H + r * h;
+#pragma unroll
+            for (int i = 0; i < HU; ++i) hv[j][i] = hr[lane + 64 * i];
+            yv[j] = Yb[r];
         }
-        s = sum64(s);
-        const float res = s - Yb[r];
-        const float g = scale * res;
-        if (lane == 0) sq[r] = res * res;
-        float *gr = Gout + r * h;
 #pragma unroll
-        for (int i = 0; i < HU; ++i) {
-            gr[lane + 64 * i] = hv[i] > 0.0f ? g * wov[i] : 0.0f;
-            acc[i] = fmaf(hv[i], g, acc[i]);
+        for (int j = 0; j < OUT_R; ++j) {
+            const int64_t r = r0 + 4 * j;
+            float s = 0.0f;
+#pragma unroll
+            for (int i = 0; i < HU; ++i) s = fmaf(hv[j][i], wov[i], s);
+            s = sum64(s);
+            if (r >= re) continue;
+            const float res = s - yv[j];
+            const float g = scale * res;
+            if (lane == 0) sq[r] = res * res;
+            float *gr = Gout + r * h;
+#pragma unroll
+            for (int i = 0; i < HU; ++i) {
+                gr[lane + 64 * i] = hv[j][i] > 0.0f ? g * wov[i] : 0.0f;
+                acc[i] = fmaf(hv[j][i], g, acc[i]);
+            }
         }
     }
 #pragma unroll
@@ -324,11 +336,22 @@ __global__ __launch_bounds__(256) void k_deep_apply(const float *__restrict__ pa
                                                     float *__restrict__ dparams, float lr, int sgd,
                                                     const float *__restrict__ sq, int64_t nb,
                                                     ReduceArgs ra) {
+    constexpr int U = 32;     // loads in flight per lane; the adds stay in index order
     if (blockIdx.x == gridDim.x - 1) {
         __shared__ float red[256];
         const int i = threadIdx.x;
         float v = 0.0f;
-        for (int64_t t = i; t < nb; t += 256) v += sq[t];
+        for (int64_t t0 = i; t0 < nb; t0 += 256 * U) {
+            float x[U];
+#pragma unroll
+            for (int j = 0; j < U; ++j) {
+                const int64_t t = t0 + 256 * j;
+                x[j] = sq[t < nb ? t : nb - 1];
+            }
+#pragma unroll
+            for (int j = 0; j < U; ++j)
+                if (t0 + 256 * j < nb) v += x[j];
+        }
         red[i] = v;
         __syncthreads();
         for (int w = 128; w >= 1; w >>= 1) {
@@ -349,16 +372,39 @@ __global__ __launch_bounds__(256) void k_deep_apply(const float *__restrict__ pa
         }
         return;
     }
+    // Segment ends are multiples of 64, so a wave lies in one segment: look it
+    // up once per wave, in scalar registers.
+    const int64_t p0 = __builtin_amdgcn_readfirstlane((int)blockIdx.x * 256 + (int)(threadIdx.x & ~63));
     const int64_t p = (int64_t)blockIdx.x * 256 + threadIdx.x;
     if (p >= np) return;
     int seg = 0;
-    while (seg + 1 < sp.nseg && p >= sp.seg_end[seg]) ++seg;
+    while (seg + 1 < sp.nseg && p0 >= sp.seg_end[seg]) ++seg;
     const int64_t start = seg == 0 ? 0 : sp.seg_end[seg - 1];
     const int64_t size = sp.seg_end[seg] - start;
+    const int n = sp.splits[seg];
     const float *q = part + sp.part_off[seg] + (p - start);
+    const float w = sgd ? params[p] : 0.0f;
     float v = 0.0f;
-    for (int z = 0; z < sp.splits[seg]; ++z) v += q[(int64_t)z * size];
-    if (sgd) params[p] -= lr * v;
+    int z0 = 0;
+    for (; z0 + U <= n; z0 += U) {
+        float x[U];
+#pragma unroll
+        for (int j = 0; j < U; ++j) x[j] = q[(int64_t)(z0 + j) * size];
+#pragma unroll
+        for (int j = 0; j < U; ++j) v += x[j];
+    }
+    for (; z0 < n; z0 += 4) {    // the last n mod U partials, four loads at a time
+        float x[4];
+#pragma unroll
+        for (int j = 0; j < 4; ++j) {
+            const int z = z0 + j < n ? z0 + j : n - 1;
+            x[j] = q[(int64_t)z * size];
+        }
+#pragma unroll
+        for (int j = 0; j < 4; ++j)
+            if (z0 + j < n) v += x[j];
+    }
+    if (sgd) params[p] = w - lr * v;
     else dparams[p] = v;
 }
 
@@ -395,7 +441,7 @@ static bool deep_shape_ok(int32_t d_in, int32_t hidden, int32_t layers) {
 // Row chunks of segment s's gradient before rounding the chunk length: a weight
 // segment W_l gets enough chunks for its GEMM to reach about 512 workgroups
 // (output tiles x chunks), at most SPLIT_MAX, with at least 64 rows a chunk; w_o
-// gets one chunk per 64 rows of the output kernel, at most OUT_CHUNKS_MAX. This
+// gets one chunk per 32 rows of the output kernel, at most OUT_CHUNKS_MAX. This
 // count never falls as nb grows, and the chunks a plan uses never exceed it, so
 // the count at max_batch sizes the partial buffer for every batch.
 static int64_t seg_chunks(int h, int L, int64_t nb, int s) {
@@ -408,7 +454,7 @@ static int64_t seg_chunks(int h, int L, int64_t nb, int s) {
         if (splits > by_rows) splits = by_rows;
         splits = splits > SPLIT_MAX ? SPLIT_MAX : splits;
     } else {
-        splits = (nb + 63) / 64;
+        splits = (nb + 31) / 32;
         splits = splits > OUT_CHUNKS_MAX ? OUT_CHUNKS_MAX : splits;
     }
     return splits < 1 ? 1 : splits;
