@@ -28,13 +28,20 @@ FP32_PEAK_TFLOPS = 157.3
 HBM_PEAK_GBS = 8000.0
 
 
-def kernel_source_hash():
+# the sources that build and launch the fused trainer (its kernel, its launch
+# planning and the headers both include)
+TRAINER_SOURCES = ("paper_2606_30497_amd/csrc/train_persistent.hip",
+                   "paper_2606_30497_amd/csrc/api.hip",
+                   "paper_2606_30497_amd/csrc/lanes.h",
+                   "paper_2606_30497_amd/csrc/mlp_internal.h",
+                   "include/mlp.h")
+
+
+def kernel_source_hash(files=TRAINER_SOURCES):
     h = hashlib.sha256()
-    csrc = os.path.join(ROOT, "paper_2606_30497_amd", "csrc")
-    for name in sorted(os.listdir(csrc)):
-        if name.endswith((".hip", ".h")):
-            with open(os.path.join(csrc, name), "rb") as f:
-                h.update(name.encode() + b"\0" + f.read())
+    for rel in files:
+        with open(os.path.join(ROOT, rel), "rb") as f:
+            h.update(rel.encode() + b"\0" + f.read())
     return h.hexdigest()[:16]
 
 
