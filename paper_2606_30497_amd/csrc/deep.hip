@@ -56,15 +56,19 @@ enum { OP_NN = 0, OP_TN = 1, OP_NT = 2 };
 enum { EP_NONE = 0, EP_RELU = 1, EP_MASK = 2 };
 
 // Global -> register staging of one K chunk: each of the 256 threads holds two
-// float4 of the a tile and two of the b tile.
+// float4 of the a tile and two of the b tile, as loaded, and whether each lies
+// inside its operand.
 struct Stage {
     float4 a[2], b[2];
+    bool oka[2], okb[2];
 };
 
-// Loads are unconditional, from an address clamped into the operand, and the
-// value is replaced by zero where the element lies outside it: a load under a
-// lane condition would compile to a branch followed by a wait for that load,
-// serialising the chunk's loads.
+// Loads are unconditional, from an address clamped into the operand: a load
+// under a lane condition would compile to a branch followed by a wait for that
+// load, serialising the chunk's loads. The values outside the operand are
+// replaced by zero only when the stage is written to LDS: a select right after
+// the load would wait for it there, and the next chunks' loads would no longer
+// overlap the current chunk's MFMAs.
 // v where ok, zeros elsewhere, component by component (a select of the whole
 // struct can be lowered through a stack slot)
 __device__ __forceinline__ float4 keep_if(bool ok, float4 v) {
@@ -82,26 +86,30 @@ __device__ __forceinline__ void gemm_fetch(Stage &st, const float *__restrict__ 
             const bool ok = k < ke && m < M;
             const float4 v = *reinterpret_cast<const float4 *>(
                 A + (k < ke ? k : ke - 1) * lda + (m < M ? m : M - 4));
-            st.a[h] = keep_if(ok, v);
+            st.a[h] = v;
+            st.oka[h] = ok;
         } else {                                  // a(m, k) = A[m lda + k]: float4 along k
             const int64_t m = m0 + (t >> 2), k = k0 + (t & 3) * 4 + 16 * h;
             const bool ok = m < M && k < ke;
             const float4 v = *reinterpret_cast<const float4 *>(
                 A + (m < M ? m : M - 1) * lda + (k < ke ? k : ke - 4));
-            st.a[h] = keep_if(ok, v);
+            st.a[h] = v;
+            st.oka[h] = ok;
         }
         if constexpr (OP == OP_NT) {              // b(k, n) = B[n ldb + k]: float4 along k
             const int64_t n = n0 + (t >> 2), k = k0 + (t & 3) * 4 + 16 * h;
             const bool ok = n < N && k < ke;
             const float4 v = *reinterpret_cast<const float4 *>(
                 B + (n < N ? n : N - 1) * ldb + (k < ke ? k : ke - 4));
-            st.b[h] = keep_if(ok, v);
+            st.b[h] = v;
+            st.okb[h] = ok;
         } else {                                  // b(k, n) = B[k ldb + n]: float4 along n
             const int64_t k = k0 + (t >> 4) + 16 * h, n = n0 + (t & 15) * 4;
             const bool ok = k < ke && n < N;
             const float4 v = *reinterpret_cast<const float4 *>(
                 B + (k < ke ? k : ke - 1) * ldb + (n < N ? n : N - 4));
-            st.b[h] = keep_if(ok, v);
+            st.b[h] = v;
+            st.okb[h] = ok;
         }
     }
 }
@@ -114,19 +122,20 @@ template <int OP>
 __device__ __forceinline__ void gemm_stash(const Stage &st, float *As, float *Bs, int t) {
 #pragma unroll
     for (int h = 0; h < 2; ++h) {
+        const float4 a = keep_if(st.oka[h], st.a[h]), b = keep_if(st.okb[h], st.b[h]);
         if constexpr (OP == OP_TN) {
-            *reinterpret_cast<float4 *>(As + ((t >> 4) + 16 * h) * GLS + (t & 15) * 4) = st.a[h];
+            *reinterpret_cast<float4 *>(As + ((t >> 4) + 16 * h) * GLS + (t & 15) * 4) = a;
         } else {
             float2 *d = reinterpret_cast<float2 *>(As + (t >> 2) * GMS + (t & 3) * 4 + 16 * h);
-            d[0] = make_float2(st.a[h].x, st.a[h].y);
-            d[1] = make_float2(st.a[h].z, st.a[h].w);
+            d[0] = make_float2(a.x, a.y);
+            d[1] = make_float2(a.z, a.w);
         }
         if constexpr (OP == OP_NT) {
             float2 *d = reinterpret_cast<float2 *>(Bs + (t >> 2) * GMS + (t & 3) * 4 + 16 * h);
-            d[0] = make_float2(st.b[h].x, st.b[h].y);
-            d[1] = make_float2(st.b[h].z, st.b[h].w);
+            d[0] = make_float2(b.x, b.y);
+            d[1] = make_float2(b.z, b.w);
         } else {
-            *reinterpret_cast<float4 *>(Bs + ((t >> 4) + 16 * h) * GLS + (t & 15) * 4) = st.b[h];
+            *reinterpret_cast<float4 *>(Bs + ((t >> 4) + 16 * h) * GLS + (t & 15) * 4) = b;
         }
     }
 }
@@ -168,6 +177,23 @@ __global__ __launch_bounds__(256) void k_gemm(const float *__restrict__ A, int l
     Stage s0, s1;
     gemm_fetch<OP>(s0, A, lda, B, ldb, M, N, m0, n0, kb, ke, t);
     if (kb + GK < ke) gemm_fetch<OP>(s1, A, lda, B, ldb, M, N, m0, n0, kb + GK, ke, t);
+    // the mask of the epilogue, loaded now (clamped addresses, no lane condition)
+    // so that its loads overlap the K loop instead of each waiting at the end
+    float gm[2][2][4];
+    if constexpr (EP == EP_MASK) {
+#pragma unroll
+        for (int i = 0; i < 2; ++i)
+#pragma unroll
+            for (int j = 0; j < 2; ++j) {
+                const int n = n0 + wn * 32 + j * 16 + li;
+                const int nc = n < N ? n : N - 1;
+#pragma unroll
+                for (int v = 0; v < 4; ++v) {
+                    const int64_t m = m0 + wm * 32 + i * 16 + 4 * lq + v;
+                    gm[i][j][v] = G[(m < M ? m : M - 1) * ldg + nc];
+                }
+            }
+    }
     auto chunk = [&](Stage &cur, int64_t kp) __attribute__((always_inline)) {
         gemm_stash<OP>(cur, As, Bs, t);
         __syncthreads();
@@ -212,7 +238,7 @@ __global__ __launch_bounds__(256) void k_gemm(const float *__restrict__ A, int l
                 if (m >= M || n >= N) continue;
                 float r = acc[i][j][v];
                 if constexpr (EP == EP_RELU) r = r > 0.0f ? r : 0.0f;           // eq. 12
-                if constexpr (EP == EP_MASK) r = G[m * ldg + n] > 0.0f ? r : 0.0f; // eq. 17
+                if constexpr (EP == EP_MASK) r = gm[i][j][v] > 0.0f ? r : 0.0f;    // eq. 17
                 Cz[m * ldc + n] = r;
             }
         }
