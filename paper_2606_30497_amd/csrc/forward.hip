@@ -48,14 +48,20 @@ struct RowTile {
     float x[8];
 };
 
+// The batch index of tile row t, loaded ahead of the rows it selects (an
+// unconditional load from a clamped address; only read for t < B).
+__device__ __forceinline__ int32_t load_index(const int32_t *__restrict__ idx, int64_t B, int64_t t) {
+    return idx ? idx[t < B ? t : B - 1] : 0;
+}
+// Rows r0 + li (t < B) of X, through the index ix loaded for them.
 __device__ __forceinline__ RowTile load_rows(const float *__restrict__ X, int64_t n_rows,
                                              const int32_t *__restrict__ idx, int64_t B, int64_t r0,
-                                             int li, int lq, int32_t *err) {
+                                             int32_t ix, int li, int lq, int32_t *err) {
     RowTile rt;
     const int64_t t = r0 + li;
     float4 a = make_float4(0.f, 0.f, 0.f, 0.f), b = a;
     if (t < B) {
-        int64_t r = idx ? (int64_t)idx[t] : t;
+        int64_t r = idx ? (int64_t)ix : t;
         if (r < 0 || r >= n_rows) {
             __hip_atomic_store(err, (int32_t)MLP_ERR_INDEX, __ATOMIC_RELAXED, __HIP_MEMORY_SCOPE_AGENT);
             r = 0;
@@ -97,12 +103,17 @@ __global__ __launch_bounds__(FWD_THREADS, FwdShape<H>::WG_PER_CU) void k_forward
     const int64_t ntiles = (B + 15) / 16;
     const int64_t iters = (ntiles + TPI - 1) / TPI;
     int64_t it = blockIdx.x;
-    RowTile cur = load_rows(X, n_rows, idx, B, (it * TPI + wt) * 16, li, lq, err);
+    const int64_t r0f = (it * TPI + wt) * 16;
+    RowTile cur = load_rows(X, n_rows, idx, B, r0f, load_index(idx, B, r0f + li), li, lq, err);
+    int32_t ixn = load_index(idx, B, ((it + gridDim.x) * TPI + wt) * 16 + li);
+    __builtin_amdgcn_s_waitcnt(0x0F70);   // vmcnt(0)
     for (; it < iters; it += gridDim.x) {
         const int64_t r0 = (it * TPI + wt) * 16;
-        // the next iteration's rows, in flight while this tile is computed
+        // the next iteration's rows, in flight while this tile is computed, and
+        // the index of the iteration after it
         const int64_t r0n = ((it + gridDim.x) * TPI + wt) * 16;
-        const RowTile nxt = load_rows(X, n_rows, idx, B, r0n, li, lq, err);
+        const RowTile nxt = load_rows(X, n_rows, idx, B, r0n, ixn, li, lq, err);
+        ixn = load_index(idx, B, ((it + 2 * (int64_t)gridDim.x) * TPI + wt) * 16 + li);
 
         // eq. 11: Z1 tile = X tile W1 (8 k steps of 4 per unit tile)
         f4 acc[NUT];
