@@ -28,8 +28,9 @@
 // GEMM tile: 64 x 64 outputs per workgroup of four waves (each 32 x 32, 2 x 2
 // v_mfma_f32_16x16x4f32 tiles), K in chunks of 32 staged in LDS k-major with a
 // row stride of 80 floats (k-major) or 34 (m-major), so that MFMA operand reads
-// are conflict-free; the next two chunks' global loads are in flight while the
-// current chunk is computed.
+// are conflict-free, alternating between two LDS buffers (one barrier per
+// chunk); the next two chunks' global loads are in flight while the current
+// chunk is computed.
 #include <hip/hip_runtime.h>
 
 #include <math.h>
@@ -48,6 +49,7 @@ constexpr int GK = 32;        // K chunk
 constexpr int GLS = 80;       // LDS row stride of a k-major operand tile ([k][m], floats)
 constexpr int GMS = 34;       // LDS row stride of an m-major operand tile ([m][k], floats)
 constexpr int GLDS = GK * GLS;   // floats per operand tile (>= GT * GMS)
+constexpr int GSTAGES = 2;    // K chunks in flight (register stages)
 constexpr int SPLIT_MAX = 64; // row chunks of a weight-gradient product
 constexpr int OUT_CHUNKS_MAX = 256;   // row chunks of the output layer (dw_o partials)
 constexpr int DEEP_MAX_LAYERS = 8;
@@ -56,23 +58,23 @@ enum { OP_NN = 0, OP_TN = 1, OP_NT = 2 };
 enum { EP_NONE = 0, EP_RELU = 1, EP_MASK = 2 };
 
 // Global -> register staging of one K chunk: each of the 256 threads holds two
-// float4 of the a tile and two of the b tile, as loaded, and whether each lies
-// inside its operand.
+// float4 of the a tile and two of the b tile.
 struct Stage {
     float4 a[2], b[2];
-    bool oka[2], okb[2];
 };
 
-// Loads are unconditional, from an address clamped into the operand: a load
-// under a lane condition would compile to a branch followed by a wait for that
-// load, serialising the chunk's loads. The values outside the operand are
-// replaced by zero only when the stage is written to LDS: a select right after
-// the load would wait for it there, and the next chunks' loads would no longer
-// overlap the current chunk's MFMAs.
-// v where ok, zeros elsewhere, component by component (a select of the whole
-// struct can be lowered through a stack slot)
-__device__ __forceinline__ float4 keep_if(bool ok, float4 v) {
-    return make_float4(ok ? v.x : 0.f, ok ? v.y : 0.f, ok ? v.z : 0.f, ok ? v.w : 0.f);
+// Sixteen zero bytes in device memory: a lane whose float4 lies outside its
+// operand loads these instead. The choice is made on the address, before the
+// load, and the loaded registers are not touched again until they are written
+// to LDS. (A load under a lane condition compiles to a branch and an immediate
+// wait for that load; a select of zero after the load is consumed, and so
+// waited for, wherever the scheduler places it, often among the MFMAs of an
+// earlier chunk. Either way the next chunks' loads stop overlapping the current
+// chunk's MFMAs.)
+__device__ __attribute__((aligned(16))) float g_zero16[4] = {0.f, 0.f, 0.f, 0.f};
+
+__device__ __forceinline__ float4 ld4(bool ok, const float *p) {
+    return *reinterpret_cast<const float4 *>(ok ? p : g_zero16);
 }
 
 template <int OP>
@@ -83,33 +85,17 @@ __device__ __forceinline__ void gemm_fetch(Stage &st, const float *__restrict__ 
     for (int h = 0; h < 2; ++h) {
         if constexpr (OP == OP_TN) {              // a(m, k) = A[k lda + m]: float4 along m
             const int64_t k = k0 + (t >> 4) + 16 * h, m = m0 + (t & 15) * 4;
-            const bool ok = k < ke && m < M;
-            const float4 v = *reinterpret_cast<const float4 *>(
-                A + (k < ke ? k : ke - 1) * lda + (m < M ? m : M - 4));
-            st.a[h] = v;
-            st.oka[h] = ok;
+            st.a[h] = ld4(k < ke && m < M, A + k * lda + m);
         } else {                                  // a(m, k) = A[m lda + k]: float4 along k
             const int64_t m = m0 + (t >> 2), k = k0 + (t & 3) * 4 + 16 * h;
-            const bool ok = m < M && k < ke;
-            const float4 v = *reinterpret_cast<const float4 *>(
-                A + (m < M ? m : M - 1) * lda + (k < ke ? k : ke - 4));
-            st.a[h] = v;
-            st.oka[h] = ok;
+            st.a[h] = ld4(m < M && k < ke, A + m * lda + k);
         }
         if constexpr (OP == OP_NT) {              // b(k, n) = B[n ldb + k]: float4 along k
             const int64_t n = n0 + (t >> 2), k = k0 + (t & 3) * 4 + 16 * h;
-            const bool ok = n < N && k < ke;
-            const float4 v = *reinterpret_cast<const float4 *>(
-                B + (n < N ? n : N - 1) * ldb + (k < ke ? k : ke - 4));
-            st.b[h] = v;
-            st.okb[h] = ok;
+            st.b[h] = ld4(n < N && k < ke, B + n * ldb + k);
         } else {                                  // b(k, n) = B[k ldb + n]: float4 along n
             const int64_t k = k0 + (t >> 4) + 16 * h, n = n0 + (t & 15) * 4;
-            const bool ok = k < ke && n < N;
-            const float4 v = *reinterpret_cast<const float4 *>(
-                B + (k < ke ? k : ke - 1) * ldb + (n < N ? n : N - 4));
-            st.b[h] = v;
-            st.okb[h] = ok;
+            st.b[h] = ld4(k < ke && n < N, B + k * ldb + n);
         }
     }
 }
@@ -122,7 +108,7 @@ template <int OP>
 __device__ __forceinline__ void gemm_stash(const Stage &st, float *As, float *Bs, int t) {
 #pragma unroll
     for (int h = 0; h < 2; ++h) {
-        const float4 a = keep_if(st.oka[h], st.a[h]), b = keep_if(st.okb[h], st.b[h]);
+        const float4 a = st.a[h], b = st.b[h];
         if constexpr (OP == OP_TN) {
             *reinterpret_cast<float4 *>(As + ((t >> 4) + 16 * h) * GLS + (t & 15) * 4) = a;
         } else {
@@ -155,8 +141,8 @@ __global__ __launch_bounds__(256) void k_gemm(const float *__restrict__ A, int l
                                               float *__restrict__ C, int ldc, int64_t c_split,
                                               int64_t M, int N, int64_t K, int64_t kc,
                                               const float *__restrict__ G, int ldg) {
-    __shared__ __attribute__((aligned(16))) float As[GLDS];
-    __shared__ __attribute__((aligned(16))) float Bs[GLDS];
+    __shared__ __attribute__((aligned(16))) float As2[2][GLDS];
+    __shared__ __attribute__((aligned(16))) float Bs2[2][GLDS];
     const int t = threadIdx.x;
     const int lane = t & 63, wave = t >> 6;
     const int li = lane & 15, lq = lane >> 4;
@@ -172,11 +158,19 @@ __global__ __launch_bounds__(256) void k_gemm(const float *__restrict__ A, int l
 #pragma unroll
         for (int j = 0; j < 2; ++j) acc[i][j] = f4{0.f, 0.f, 0.f, 0.f};
 
-    // two chunks in flight: chunk c + 2 is fetched into the registers chunk c
-    // has just left, while chunk c is on the matrix cores
-    Stage s0, s1;
-    gemm_fetch<OP>(s0, A, lda, B, ldb, M, N, m0, n0, kb, ke, t);
-    if (kb + GK < ke) gemm_fetch<OP>(s1, A, lda, B, ldb, M, N, m0, n0, kb + GK, ke, t);
+    // GSTAGES chunks in flight: chunk c + GSTAGES is fetched into the registers
+    // chunk c has just left, while chunk c is on the matrix cores. Chunks
+    // alternate between two LDS buffers, so one barrier per chunk suffices: the
+    // buffer a chunk is written to was last read by the chunk before the
+    // previous barrier, which every wave has passed. Every pass of
+    // the main loop issues the same loads (the fetches past the last chunk read
+    // the zero block and are never stashed), so the compiler can wait for each
+    // stage's own loads only, not for all loads in flight.
+    const int64_t nch = (ke - kb + GK - 1) / GK;
+    Stage st[GSTAGES];
+#pragma unroll
+    for (int q = 0; q < GSTAGES; ++q)
+        gemm_fetch<OP>(st[q], A, lda, B, ldb, M, N, m0, n0, kb + q * GK, ke, t);
     // the mask of the epilogue, loaded now (clamped addresses, no lane condition)
     // so that its loads overlap the K loop instead of each waiting at the end
     float gm[2][2][4];
@@ -194,10 +188,8 @@ __global__ __launch_bounds__(256) void k_gemm(const float *__restrict__ A, int l
                 }
             }
     }
-    auto chunk = [&](Stage &cur, int64_t kp) __attribute__((always_inline)) {
-        gemm_stash<OP>(cur, As, Bs, t);
-        __syncthreads();
-        if (kp + 2 * GK < ke) gemm_fetch<OP>(cur, A, lda, B, ldb, M, N, m0, n0, kp + 2 * GK, ke, t);
+    auto mfma_chunk = [&](int buf) __attribute__((always_inline)) {
+        const float *As = As2[buf], *Bs = Bs2[buf];
         // eight k steps of 4 on the matrix cores
 #pragma unroll
         for (int ks = 0; ks < GK / 4; ++ks) {
@@ -219,11 +211,27 @@ __global__ __launch_bounds__(256) void k_gemm(const float *__restrict__ A, int l
                 for (int j = 0; j < 2; ++j)
                     acc[i][j] = __builtin_amdgcn_mfma_f32_16x16x4f32(a[i], b[j], acc[i][j], 0, 0, 0);
         }
-        __syncthreads();
     };
-    for (int64_t k0 = kb; k0 < ke; k0 += 2 * GK) {
-        chunk(s0, k0);
-        if (k0 + GK < ke) chunk(s1, k0 + GK);
+    int64_t c = 0;
+    for (; c + GSTAGES <= nch; c += GSTAGES) {
+#pragma unroll
+        for (int q = 0; q < GSTAGES; ++q) {
+            const int buf = (int)((c + q) & 1);
+            gemm_stash<OP>(st[q], As2[buf], Bs2[buf], t);
+            __syncthreads();
+            gemm_fetch<OP>(st[q], A, lda, B, ldb, M, N, m0, n0, kb + (c + q + GSTAGES) * GK, ke, t);
+            mfma_chunk(buf);
+        }
+    }
+    // the last nch - c < GSTAGES chunks, already in registers
+#pragma unroll
+    for (int q = 0; q < GSTAGES - 1; ++q) {
+        if (c + q < nch) {
+            const int buf = (int)((c + q) & 1);
+            gemm_stash<OP>(st[q], As2[buf], Bs2[buf], t);
+            __syncthreads();
+            mfma_chunk(buf);
+        }
     }
     // ---- epilogue: lane holds C[4 lq + v][li] of each 16 x 16 tile ----
     float *Cz = C + (int64_t)blockIdx.z * c_split;
