@@ -49,7 +49,8 @@ constexpr int GK = 32;        // K chunk
 constexpr int GLS = 80;       // LDS row stride of a k-major operand tile ([k][m], floats)
 constexpr int GMS = 34;       // LDS row stride of an m-major operand tile ([m][k], floats)
 constexpr int GLDS = GK * GLS;   // floats per operand tile (>= GT * GMS)
-constexpr int GSTAGES = 2;    // K chunks in flight (register stages)
+constexpr int GSTAGES = 2;    // K chunks in flight (register stages; 3 or 4 measured slower)
+constexpr int GEMM_CUS = 256; // compute units the tile choice plans for
 constexpr int SPLIT_MAX = 64; // row chunks of a weight-gradient product
 constexpr int OUT_CHUNKS_MAX = 256;   // row chunks of the output layer (dw_o partials)
 constexpr int DEEP_MAX_LAYERS = 8;
@@ -57,10 +58,12 @@ constexpr int DEEP_MAX_LAYERS = 8;
 enum { OP_NN = 0, OP_TN = 1, OP_NT = 2 };
 enum { EP_NONE = 0, EP_RELU = 1, EP_MASK = 2 };
 
-// Global -> register staging of one K chunk: each of the 256 threads holds two
-// float4 of the a tile and two of the b tile.
+// Global -> register staging of one K chunk of a TM x 64 output tile: each of
+// the 256 threads holds TM / 32 float4 of the a tile ([TM x 32]) and two of the
+// b tile ([32 x 64]).
+template <int TM>
 struct Stage {
-    float4 a[2], b[2];
+    float4 a[TM / 32], b[2];
 };
 
 // Sixteen zero bytes in device memory: a lane whose float4 lies outside its
@@ -77,19 +80,26 @@ __device__ __forceinline__ float4 ld4(bool ok, const float *p) {
     return *reinterpret_cast<const float4 *>(ok ? p : g_zero16);
 }
 
-template <int OP>
-__device__ __forceinline__ void gemm_fetch(Stage &st, const float *__restrict__ A, int lda,
+// Thread t's float4 h of an a tile: loaded along m (k-major, TN) it is
+// (k, m) = (t / (TM/4) + (1024/TM) h, 4 (t % (TM/4))); loaded along k
+// (m-major) it is (m, k) = (t / (256/TM), 4 (t % (256/TM)) + (1024/TM) h).
+// The b tile is the TM = 64 case of the same maps with n for m.
+template <int OP, int TM>
+__device__ __forceinline__ void gemm_fetch(Stage<TM> &st, const float *__restrict__ A, int lda,
                                            const float *__restrict__ B, int ldb, int64_t M, int N,
                                            int64_t m0, int n0, int64_t k0, int64_t ke, int t) {
 #pragma unroll
-    for (int h = 0; h < 2; ++h) {
+    for (int h = 0; h < TM / 32; ++h) {
         if constexpr (OP == OP_TN) {              // a(m, k) = A[k lda + m]: float4 along m
-            const int64_t k = k0 + (t >> 4) + 16 * h, m = m0 + (t & 15) * 4;
+            const int64_t k = k0 + t / (TM / 4) + (1024 / TM) * h, m = m0 + (t % (TM / 4)) * 4;
             st.a[h] = ld4(k < ke && m < M, A + k * lda + m);
         } else {                                  // a(m, k) = A[m lda + k]: float4 along k
-            const int64_t m = m0 + (t >> 2), k = k0 + (t & 3) * 4 + 16 * h;
+            const int64_t m = m0 + t / (256 / TM), k = k0 + (t % (256 / TM)) * 4 + (1024 / TM) * h;
             st.a[h] = ld4(m < M && k < ke, A + m * lda + k);
         }
+    }
+#pragma unroll
+    for (int h = 0; h < 2; ++h) {
         if constexpr (OP == OP_NT) {              // b(k, n) = B[n ldb + k]: float4 along k
             const int64_t n = n0 + (t >> 2), k = k0 + (t & 3) * 4 + 16 * h;
             st.b[h] = ld4(n < N && k < ke, B + n * ldb + k);
@@ -104,18 +114,23 @@ __device__ __forceinline__ void gemm_fetch(Stage &st, const float *__restrict__ 
 // ([k][m], stride GLS); one loaded along k is stored as loaded, m-major
 // ([m][k], stride GMS = 34: the 16 m rows x 2 k columns an MFMA operand read
 // touches per half wave land in 32 distinct banks).
-template <int OP>
-__device__ __forceinline__ void gemm_stash(const Stage &st, float *As, float *Bs, int t) {
+template <int OP, int TM>
+__device__ __forceinline__ void gemm_stash(const Stage<TM> &st, float *As, float *Bs, int t) {
 #pragma unroll
-    for (int h = 0; h < 2; ++h) {
-        const float4 a = st.a[h], b = st.b[h];
+    for (int h = 0; h < TM / 32; ++h) {
+        const float4 a = st.a[h];
         if constexpr (OP == OP_TN) {
-            *reinterpret_cast<float4 *>(As + ((t >> 4) + 16 * h) * GLS + (t & 15) * 4) = a;
+            *reinterpret_cast<float4 *>(As + (t / (TM / 4) + (1024 / TM) * h) * GLS + (t % (TM / 4)) * 4) = a;
         } else {
-            float2 *d = reinterpret_cast<float2 *>(As + (t >> 2) * GMS + (t & 3) * 4 + 16 * h);
+            float2 *d = reinterpret_cast<float2 *>(As + (t / (256 / TM)) * GMS + (t % (256 / TM)) * 4 +
+                                                   (1024 / TM) * h);
             d[0] = make_float2(a.x, a.y);
             d[1] = make_float2(a.z, a.w);
         }
+    }
+#pragma unroll
+    for (int h = 0; h < 2; ++h) {
+        const float4 b = st.b[h];
         if constexpr (OP == OP_NT) {
             float2 *d = reinterpret_cast<float2 *>(Bs + (t >> 2) * GMS + (t & 3) * 4 + 16 * h);
             d[0] = make_float2(b.x, b.y);
@@ -130,12 +145,14 @@ __device__ __forceinline__ void gemm_stash(const Stage &st, float *As, float *Bs
 //   NN: a(m, k) = A[m lda + k],  b(k, n) = B[k ldb + n]
 //   TN: a(m, k) = A[k lda + m],  b(k, n) = B[k ldb + n]
 //   NT: a(m, k) = A[m lda + k],  b(k, n) = B[n ldb + k]
-// Grid: (ceil(M/64), ceil(N/64), splits); split z covers k in [z kc, min(K, z kc + kc))
+// Output tile TM x 64 (TM = 64 or 32; each of the four waves computes a
+// TM/2 x 32 quarter). Grid: (ceil(M/TM), ceil(N/64), splits); split z covers k
+// in [z kc, min(K, z kc + kc))
 // and writes C + z * c_split. N and the contiguous dimension of every operand
 // are multiples of 16 (hidden widths and d_in); M and K are arbitrary. The next
 // two K chunks are loaded into registers while the current one is on the matrix
 // cores.
-template <int OP, int EP>
+template <int OP, int EP, int TM>
 __global__ __launch_bounds__(256) void k_gemm(const float *__restrict__ A, int lda,
                                               const float *__restrict__ B, int ldb,
                                               float *__restrict__ C, int ldc, int64_t c_split,
@@ -147,18 +164,19 @@ __global__ __launch_bounds__(256) void k_gemm(const float *__restrict__ A, int l
     const int lane = t & 63, wave = t >> 6;
     const int li = lane & 15, lq = lane >> 4;
     const int wm = wave >> 1, wn = wave & 1;
-    const int64_t m0 = (int64_t)blockIdx.x * GT;
+    constexpr int MI = TM / 32;   // 16-row MFMA tiles per wave
+    const int64_t m0 = (int64_t)blockIdx.x * TM;
     const int n0 = blockIdx.y * GT;
     const int64_t kb = (int64_t)blockIdx.z * kc;
     const int64_t ke = kb + kc < K ? kb + kc : K;
 
-    f4 acc[2][2];
+    f4 acc[MI][2];
 #pragma unroll
-    for (int i = 0; i < 2; ++i)
+    for (int i = 0; i < MI; ++i)
 #pragma unroll
         for (int j = 0; j < 2; ++j) acc[i][j] = f4{0.f, 0.f, 0.f, 0.f};
 
-    // GSTAGES chunks in flight: chunk c + GSTAGES is fetched into the registers
+    // NS chunks in flight: chunk c + NS is fetched into the registers
     // chunk c has just left, while chunk c is on the matrix cores. Chunks
     // alternate between two LDS buffers, so one barrier per chunk suffices: the
     // buffer a chunk is written to was last read by the chunk before the
@@ -166,24 +184,25 @@ __global__ __launch_bounds__(256) void k_gemm(const float *__restrict__ A, int l
     // the main loop issues the same loads (the fetches past the last chunk read
     // the zero block and are never stashed), so the compiler can wait for each
     // stage's own loads only, not for all loads in flight.
+    constexpr int NS = GSTAGES;
     const int64_t nch = (ke - kb + GK - 1) / GK;
-    Stage st[GSTAGES];
+    Stage<TM> st[NS];
 #pragma unroll
-    for (int q = 0; q < GSTAGES; ++q)
-        gemm_fetch<OP>(st[q], A, lda, B, ldb, M, N, m0, n0, kb + q * GK, ke, t);
+    for (int q = 0; q < NS; ++q)
+        gemm_fetch<OP, TM>(st[q], A, lda, B, ldb, M, N, m0, n0, kb + q * GK, ke, t);
     // the mask of the epilogue, loaded now (clamped addresses, no lane condition)
     // so that its loads overlap the K loop instead of each waiting at the end
-    float gm[2][2][4];
+    float gm[MI][2][4];
     if constexpr (EP == EP_MASK) {
 #pragma unroll
-        for (int i = 0; i < 2; ++i)
+        for (int i = 0; i < MI; ++i)
 #pragma unroll
             for (int j = 0; j < 2; ++j) {
                 const int n = n0 + wn * 32 + j * 16 + li;
                 const int nc = n < N ? n : N - 1;
 #pragma unroll
                 for (int v = 0; v < 4; ++v) {
-                    const int64_t m = m0 + wm * 32 + i * 16 + 4 * lq + v;
+                    const int64_t m = m0 + wm * (TM / 2) + i * 16 + 4 * lq + v;
                     gm[i][j][v] = G[(m < M ? m : M - 1) * ldg + nc];
                 }
             }
@@ -194,10 +213,10 @@ __global__ __launch_bounds__(256) void k_gemm(const float *__restrict__ A, int l
 #pragma unroll
         for (int ks = 0; ks < GK / 4; ++ks) {
             const int kr = ks * 4 + lq;
-            float a[2], b[2];
+            float a[MI], b[2];
 #pragma unroll
-            for (int i = 0; i < 2; ++i) {
-                const int m = wm * 32 + i * 16 + li;
+            for (int i = 0; i < MI; ++i) {
+                const int m = wm * (TM / 2) + i * 16 + li;
                 a[i] = OP == OP_TN ? As[kr * GLS + m] : As[m * GMS + kr];
             }
 #pragma unroll
@@ -206,29 +225,29 @@ __global__ __launch_bounds__(256) void k_gemm(const float *__restrict__ A, int l
                 b[j] = OP == OP_NT ? Bs[n * GMS + kr] : Bs[kr * GLS + n];
             }
 #pragma unroll
-            for (int i = 0; i < 2; ++i)
+            for (int i = 0; i < MI; ++i)
 #pragma unroll
                 for (int j = 0; j < 2; ++j)
                     acc[i][j] = __builtin_amdgcn_mfma_f32_16x16x4f32(a[i], b[j], acc[i][j], 0, 0, 0);
         }
     };
     int64_t c = 0;
-    for (; c + GSTAGES <= nch; c += GSTAGES) {
+    for (; c + NS <= nch; c += NS) {
 #pragma unroll
-        for (int q = 0; q < GSTAGES; ++q) {
+        for (int q = 0; q < NS; ++q) {
             const int buf = (int)((c + q) & 1);
-            gemm_stash<OP>(st[q], As2[buf], Bs2[buf], t);
+            gemm_stash<OP, TM>(st[q], As2[buf], Bs2[buf], t);
             __syncthreads();
-            gemm_fetch<OP>(st[q], A, lda, B, ldb, M, N, m0, n0, kb + (c + q + GSTAGES) * GK, ke, t);
+            gemm_fetch<OP, TM>(st[q], A, lda, B, ldb, M, N, m0, n0, kb + (c + q + NS) * GK, ke, t);
             mfma_chunk(buf);
         }
     }
-    // the last nch - c < GSTAGES chunks, already in registers
+    // the last nch - c < NS chunks, already in registers
 #pragma unroll
-    for (int q = 0; q < GSTAGES - 1; ++q) {
+    for (int q = 0; q < NS - 1; ++q) {
         if (c + q < nch) {
             const int buf = (int)((c + q) & 1);
-            gemm_stash<OP>(st[q], As2[buf], Bs2[buf], t);
+            gemm_stash<OP, TM>(st[q], As2[buf], Bs2[buf], t);
             __syncthreads();
             mfma_chunk(buf);
         }
@@ -236,13 +255,13 @@ __global__ __launch_bounds__(256) void k_gemm(const float *__restrict__ A, int l
     // ---- epilogue: lane holds C[4 lq + v][li] of each 16 x 16 tile ----
     float *Cz = C + (int64_t)blockIdx.z * c_split;
 #pragma unroll
-    for (int i = 0; i < 2; ++i)
+    for (int i = 0; i < MI; ++i)
 #pragma unroll
         for (int j = 0; j < 2; ++j) {
             const int n = n0 + wn * 32 + j * 16 + li;
 #pragma unroll
             for (int v = 0; v < 4; ++v) {
-                const int64_t m = m0 + wm * 32 + i * 16 + 4 * lq + v;
+                const int64_t m = m0 + wm * (TM / 2) + i * 16 + 4 * lq + v;
                 if (m >= M || n >= N) continue;
                 float r = acc[i][j][v];
                 if constexpr (EP == EP_RELU) r = r > 0.0f ? r : 0.0f;           // eq. 12
@@ -529,13 +548,23 @@ static size_t deep_ws_floats(int h, int L, int64_t mb) {
            (size_t)(L + 2) * pad64f(b * (size_t)h) + (size_t)part_floats(h, L, mb);
 }
 
+// 32-row tiles when 64-row ones would leave fewer than two workgroups per CU
+// (the 256-wide layers: one 64 x 64 tile per CU leaves one wave per SIMD), or
+// when M itself is 32 (the weight gradient of W_1).
 template <int OP, int EP>
 static hipError_t gemm(hipStream_t st, const float *A, int lda, const float *B, int ldb, float *C,
                        int ldc, int64_t c_split, int64_t M, int N, int64_t K, int splits,
                        int64_t kc, const float *G = nullptr, int ldg = 0) {
-    const dim3 grid((unsigned)((M + GT - 1) / GT), (unsigned)((N + GT - 1) / GT), (unsigned)splits);
-    hipLaunchKernelGGL((k_gemm<OP, EP>), grid, dim3(256), 0, st, A, lda, B, ldb, C, ldc, c_split, M,
-                       N, K, kc, G, ldg);
+    const int64_t tiles64 = ((M + GT - 1) / GT) * ((N + GT - 1) / GT) * splits;
+    const bool small = M <= 32 || tiles64 < 2 * GEMM_CUS;
+    const int tm = small ? 32 : GT;
+    const dim3 grid((unsigned)((M + tm - 1) / tm), (unsigned)((N + GT - 1) / GT), (unsigned)splits);
+    if (small)
+        hipLaunchKernelGGL((k_gemm<OP, EP, 32>), grid, dim3(256), 0, st, A, lda, B, ldb, C, ldc,
+                           c_split, M, N, K, kc, G, ldg);
+    else
+        hipLaunchKernelGGL((k_gemm<OP, EP, GT>), grid, dim3(256), 0, st, A, lda, B, ldb, C, ldc,
+                           c_split, M, N, K, kc, G, ldg);
     return hipGetLastError();
 }
 
