@@ -131,6 +131,29 @@ def test_gradients_gaussian(mlp, h, L, B):
     assert abs(float(loss.cpu()[0]) - rL) <= 1e-5 * rL
 
 
+def test_large_tiles(mlp):
+    """h = 1024 at a batch of 2100 rows: the forward and back-propagation
+    products run 64-row tiles (33 x 16 of them, the last one 52 rows deep) and
+    the W_2 gradient two row chunks of 64-row tiles, the launch shapes of the
+    1024-wide evaluation net (smaller batches run 32-row tiles). Gradients and
+    loss against the oracle as in the other Gaussian cases; the forward of all
+    2100 rows on sampled rows."""
+    h, L, B = 1024, 2, 2100
+    rng = np.random.default_rng(21)
+    d = datagen.make_data(5000, 32, seed=6, with_perm=False)
+    P = _gauss_net(rng, h, L)
+    ctx, _ = _ctx(mlp, P, h, L, B)
+    idx = rng.integers(0, 5000, size=B).astype(np.int32)
+    dP, loss = mlp.mlp_deep_backward(ctx, _to(d.X), _to(d.Y), _to(idx))
+    ref, rL, _ = oracle.deep_grad(d.X, d.Y, P, D, h, L, idx=idx)
+    assert rel(dP.cpu().numpy(), ref) <= 1e-3
+    assert abs(float(loss.cpu()[0]) - rL) <= 1e-5 * rL
+    got = mlp.mlp_deep_forward(ctx, _to(d.X), _to(idx)).cpu().numpy()
+    rows = np.arange(0, B, 7)
+    assert rel(got[rows], oracle.deep_forward(d.X, P, D, h, L, idx=idx[rows])) < 1e-5
+    mlp.mlp_deep_check_errors(ctx)
+
+
 @pytest.mark.parametrize("h", [64, 256])
 def test_one_layer_meets_the_main_bar(mlp, h):
     """L = 1 is the paper's network: gradients within 1e-4 of the shallow oracle
