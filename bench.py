@@ -211,6 +211,18 @@ def measure_forward(h, X, args, mlp, torch, np):
     ms = float(np.mean([e0.elapsed_time(e1) for e0, e1 in ev]))
     flop = 66.0 * h * n
     achieved = flop / (ms / 1e3) / 1e12
+    gbs = 132.0 * n / (ms / 1e3) / 1e9
+    # the bound is the side of the ridge the arithmetic intensity (66 h FLOP per
+    # 132 bytes) falls on: HBM at h = 32 (16 FLOP/B), the matrix cores above
+    if 66.0 * h / 132.0 < FP32_PEAK_TFLOPS * 1e3 / HBM_PEAK_GBS:
+        roof = {"bound": "hbm", "achieved": gbs, "peak": HBM_PEAK_GBS, "unit": "GB/s",
+                "frac": gbs / HBM_PEAK_GBS, "traffic": None,
+                "tflops": achieved, "tflops_frac": achieved / FP32_PEAK_TFLOPS}
+    else:
+        roof = {"bound": "mfma", "achieved": achieved, "peak": FP32_PEAK_TFLOPS,
+                "unit": "TFLOP/s", "frac": achieved / FP32_PEAK_TFLOPS,
+                "hbm_gbs": gbs, "hbm_frac": gbs / HBM_PEAK_GBS}
+    roof.update({"kernel_ms": ms, "flop_per_launch": flop})
     extra = {}
     if not args.no_cpu_baseline:
         import oracle
@@ -234,11 +246,7 @@ def measure_forward(h, X, args, mlp, torch, np):
         "dtype": "f32",
         "data": "synthetic",
         "config": {"workload": "forward_mlp32-%d-1_n%d" % (h, n), "hidden": h, "n": n},
-        "roofline": {"bound": "mfma", "achieved": achieved, "peak": FP32_PEAK_TFLOPS,
-                     "unit": "TFLOP/s", "frac": achieved / FP32_PEAK_TFLOPS,
-                     "kernel_ms": ms, "flop_per_launch": flop,
-                     "hbm_gbs": 132.0 * n / (ms / 1e3) / 1e9,
-                     "hbm_frac": 132.0 * n / (ms / 1e3) / 1e9 / HBM_PEAK_GBS},
+        "roofline": roof,
     }, **extra)
 
 
