@@ -117,7 +117,7 @@ def test_gradients_dyadic(mlp, h, L, B):
     assert abs(float(loss.cpu()[0]) - rL) <= 1e-5 * max(rL, 1e-30)
 
 
-@pytest.mark.parametrize("h,L", [(64, 2), (256, 2), (256, 3)])
+@pytest.mark.parametrize("h,L", [(64, 2), (256, 2), (256, 3), (64, 8), (128, 8)])
 @pytest.mark.parametrize("B", [7, 160, 1000])
 def test_gradients_gaussian(mlp, h, L, B):
     rng = np.random.default_rng(h * L + B)
@@ -202,6 +202,23 @@ def test_train_epochs_with_shuffle_and_tail(mlp, h, L):
     assert rel(gP - P0, ref["P"] - P0) <= 1e-3
     assert np.all(np.abs(gsl - ref["step_loss"]) <= 1e-3 * ref["step_loss"])
     assert np.all(np.abs(gel - ref["epoch_loss"]) <= 1e-3 * ref["epoch_loss"])
+
+
+def test_train_eight_layers(mlp):
+    """The deepest net the API takes (L = 8, h = 64), two shuffled epochs of
+    1500 rows at batch 256 (tail of 220) on the evaluation recipe. The oracle
+    itself moves by under 1e-6 when W0 is perturbed by 1e-7, so the bars are
+    those of the one-layer path."""
+    h, L, B, lr, E = 64, 8, 256, 0.002, 2
+    d = datagen.make_data(1500, 32, epochs=E, seed=1005)
+    P = _gauss_net(np.random.default_rng(9), h, L)
+    gP, gsl, gel = _train(mlp, d.X, d.Y, P, h, L, B, lr, E, perm=d.perm)
+    ref = oracle.deep_train(d.X, d.Y, P, D, h, L, B, lr, E, perm=d.perm)
+    assert ref["steps"] == 12 and len(gsl) == 12
+    P0 = P.astype(np.float64)
+    assert rel(gP - P0, ref["P"] - P0) <= 1e-3
+    assert np.all(np.abs(gsl - ref["step_loss"]) <= 1e-4 * ref["step_loss"])
+    assert np.all(np.abs(gel - ref["epoch_loss"]) <= 1e-4 * ref["epoch_loss"])
 
 
 def test_train_gaussian_workload_batch(mlp):
