@@ -996,6 +996,14 @@ static const TrainPlan *all_plans(int *count) {
     return plans;
 }
 
+// Test and diagnostic hooks, read from the environment (none skips work):
+//   MLP_PX=p, MLP_INST=i   restrict the choice to shapes with PX = p, or to
+//                          instance i (the parity tests run every instantiated
+//                          shape this way);
+//   MLP_FORCE_COHERENT=1   device-coherent exchange stores even when every group
+//                          sits on one XCD (tested bitwise against the default);
+//   MLP_TRACE=1 / 2        per-phase s_memrealtime stamps of one workgroup / of
+//                          every workgroup into the workspace (timing analysis).
 bool plan_train(int hidden, int64_t batch, TrainPlan *plan) {
     const char *force = getenv("MLP_PX");
     const int fpx = force ? atoi(force) : 0;
