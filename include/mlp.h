@@ -51,6 +51,7 @@ typedef enum {
     MLP_ERR_UNSUPPORTED = -2,  /* d_in != 32, d_out != 1, hidden not supported   */
     MLP_ERR_WORKSPACE = -3,    /* workspace too small or misaligned              */
     MLP_ERR_HIP = -4,          /* a HIP runtime call or kernel launch failed     */
+    MLP_ERR_NONFINITE = -5,    /* a batch loss was NaN or infinite (diverged)    */
     MLP_ERR_INDEX = -6,        /* a kernel met a row index outside [0, n_rows)   */
     MLP_ERR_TIMEOUT = -7       /* a wait inside the training kernel timed out    */
 } mlp_status;
@@ -159,7 +160,11 @@ mlp_status mlp_train_epochs(mlp_t ctx, const float *X, const float *Y, int64_t n
                             float *epoch_loss, float *step_loss);
 
 /* Synchronise the stream and report sticky kernel-side errors (MLP_ERR_INDEX,
- * MLP_ERR_TIMEOUT) raised since the last check; clears them. */
+ * MLP_ERR_TIMEOUT, MLP_ERR_NONFINITE) raised since the last check; clears them.
+ * MLP_ERR_NONFINITE means some batch loss of a training or gradient call was
+ * NaN or infinite (training diverged); the computation itself is not stopped,
+ * and non-finite values propagate as fp32 arithmetic makes them. When several
+ * errors were raised, the one reported is the last written. */
 mlp_status mlp_check_errors(mlp_t ctx);
 
 /* Timing of the training kernel. When enabled, mlp_train_epochs and
@@ -238,7 +243,8 @@ mlp_status mlp_deep_train_epochs(mlp_deep_t ctx, const float *X, const float *Y,
                                  int64_t batch, float lr, int32_t epochs, const int32_t *perm,
                                  int64_t max_steps, float *epoch_loss, float *step_loss);
 
-/* Synchronise and report (then clear) a sticky MLP_ERR_INDEX. */
+/* Synchronise and report (then clear) a sticky MLP_ERR_INDEX or MLP_ERR_NONFINITE
+ * (as mlp_check_errors). */
 mlp_status mlp_deep_check_errors(mlp_deep_t ctx);
 
 /* HIP-event timing of the last mlp_deep_sgd_step / mlp_deep_train_epochs call

@@ -49,6 +49,7 @@ extern "C" const char *mlp_status_string(mlp_status s) {
     case MLP_ERR_HIP: return "HIP runtime error";
     case MLP_ERR_INDEX: return "row index out of range";
     case MLP_ERR_TIMEOUT: return "a wait in the training kernel timed out";
+    case MLP_ERR_NONFINITE: return "a batch loss was NaN or infinite";
     }
     return "unknown status";
 }
@@ -311,7 +312,8 @@ extern "C" mlp_status mlp_check_errors(mlp_t c) {
     if (err) {
         if (clear_control(*c) != hipSuccess || hipStreamSynchronize(c->stream) != hipSuccess)
             return MLP_ERR_HIP;
-        return err == MLP_ERR_TIMEOUT ? MLP_ERR_TIMEOUT : MLP_ERR_INDEX;
+        if (err == MLP_ERR_TIMEOUT || err == MLP_ERR_NONFINITE) return (mlp_status)err;
+        return MLP_ERR_INDEX;
     }
     return MLP_OK;
 }

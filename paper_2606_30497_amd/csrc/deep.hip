@@ -414,6 +414,7 @@ __global__ __launch_bounds__(256) void k_deep_apply(const float *__restrict__ pa
         if (i == 0) {
             const float sse = red[0];
             const float L = sse * ra.inv_nb;
+            flag_nonfinite(sse, &ra.ctl->err);
             if (ra.loss) ra.loss[0] = L;
             if (ra.step_loss) ra.step_loss[ra.step] = L;
             if (ra.epoch_loss) {
@@ -836,7 +837,7 @@ extern "C" mlp_status mlp_deep_check_errors(mlp_deep_t c) {
         tmp.stream = c->stream;
         if (clear_control(tmp) != hipSuccess || hipStreamSynchronize(c->stream) != hipSuccess)
             return MLP_ERR_HIP;
-        return MLP_ERR_INDEX;
+        return err == MLP_ERR_NONFINITE ? MLP_ERR_NONFINITE : MLP_ERR_INDEX;
     }
     return MLP_OK;
 }

@@ -84,6 +84,7 @@ __global__ __launch_bounds__(256) void k_hl_loss(const float *__restrict__ sq, i
     if (i == 0) {
         const float sse = part[0];
         const float L = sse * a.inv_nb;
+        flag_nonfinite(sse, &a.ctl->err);
         if (a.loss) a.loss[0] = L;
         if (a.step_loss) a.step_loss[a.step] = L;
         if (a.epoch_loss) {

@@ -159,6 +159,7 @@ __global__ __launch_bounds__(256) void k_reduce(const float *__restrict__ partia
         else a.dW2[t - N1] = s;
     } else {
         const float L = s * a.inv_nb;                                            // eq. 14
+        flag_nonfinite(s, &a.ctl->err);
         if (a.loss) a.loss[0] = L;
         if (a.step_loss) a.step_loss[a.step] = L;
         if (a.epoch_loss) {

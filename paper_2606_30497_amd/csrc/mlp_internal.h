@@ -16,6 +16,13 @@ constexpr size_t CTL_BYTES = 4096;
 
 constexpr int32_t MLP_ERR_TIMEOUT_CODE = MLP_ERR_TIMEOUT;
 
+// Raise the sticky MLP_ERR_NONFINITE when a batch's sum of squared residuals is
+// NaN or infinite (the comparison is false for NaN).
+__device__ __forceinline__ void flag_nonfinite(float sse, int32_t *err) {
+    if (!(fabsf(sse) <= 3.40282347e38f))
+        __hip_atomic_store(err, (int32_t)MLP_ERR_NONFINITE, __ATOMIC_RELAXED, __HIP_MEMORY_SCOPE_AGENT);
+}
+
 // Control words at the head of the workspace.
 struct Control {
     int32_t err;          // sticky kernel-side error (an mlp_status code)

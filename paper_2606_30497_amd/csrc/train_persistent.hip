@@ -547,6 +547,7 @@ __global__ __launch_bounds__(NTHR) void k_train(const TrainArgs a) {
                     wt.settle(sw, tag_prev, [&](int) { return lane < PR ? ld1(rB, sse_prev) : pack(0.f, tag_prev); });
                     const float sse = sum64(lane < PR ? val_of(sw[0]) : 0.0f);
                     if (lane == 0) {
+                        flag_nonfinite(sse, COLD(err));
                         const float L = sse / (float)nb_prev;               // eq. 14
                         float *lo = COLD(loss), *sl = COLD(step_loss), *el = COLD(epoch_loss);
                         if (lo) lo[0] = L;
@@ -769,6 +770,7 @@ __global__ __launch_bounds__(NTHR) void k_train(const TrainArgs a) {
                 wt.settle(swl, tag_last, reload);
                 const float sse = sum64(lane < PR ? val_of(swl[0]) : 0.0f);
                 if (lane == 0) {
+                    flag_nonfinite(sse, COLD(err));
                     const float L = sse / (float)nb_prev;
                     float *lo = COLD(loss), *sl = COLD(step_loss), *el = COLD(epoch_loss);
                     if (lo) lo[0] = L;

@@ -21,7 +21,8 @@ MAX_BATCH = 1 << 20
 
 MLP_OK = 0
 STATUS = {0: "MLP_OK", -1: "MLP_ERR_INVALID_ARG", -2: "MLP_ERR_UNSUPPORTED",
-          -3: "MLP_ERR_WORKSPACE", -4: "MLP_ERR_HIP", -6: "MLP_ERR_INDEX"}
+          -3: "MLP_ERR_WORKSPACE", -4: "MLP_ERR_HIP", -5: "MLP_ERR_NONFINITE",
+          -6: "MLP_ERR_INDEX", -7: "MLP_ERR_TIMEOUT"}
 
 STRATEGY_FUSED, STRATEGY_TILE, STRATEGY_OPTIMIZED, STRATEGY_BASELINE = 0, 1, 2, 3
 STRATEGIES = {"fused": STRATEGY_FUSED, "tile": STRATEGY_TILE, "optimized": STRATEGY_OPTIMIZED,

@@ -84,10 +84,22 @@ def test_deep_sizes_and_checks():
     assert lib.mlp_deep_check_errors(None) == -1
 
 
+def declared_statuses():
+    text = re.sub(r"/\*.*?\*/", "", open(HEADER).read(), flags=re.S)
+    return {name: int(v) for name, v in re.findall(r"\b(MLP_(?:OK|ERR_[A-Z_]+))\s*=\s*(-?\d+)", text)}
+
+
 def test_status_strings():
+    """Every status the header declares has a message in the library and its
+    name in the binding."""
     lib = _lib()
-    for s in (0, -1, -2, -3, -4, -6):
-        assert lib.mlp_status_string(s)
+    from paper_2606_30497_amd import mlp
+    codes = declared_statuses()
+    assert codes["MLP_OK"] == 0 and codes["MLP_ERR_NONFINITE"] == -5
+    assert len(set(codes.values())) == len(codes)
+    for name, v in codes.items():
+        assert lib.mlp_status_string(v) != b"unknown status", name
+        assert mlp.STATUS[v] == name
     assert lib.mlp_status_string(-99) == b"unknown status"
 
 

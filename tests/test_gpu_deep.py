@@ -269,3 +269,17 @@ def test_errors(mlp):
                                      None, -1, None, None) == -1
     torch.cuda.synchronize()
     assert torch.equal(before, p)
+
+
+def test_divergence_is_flagged(mlp):
+    """As in the one-layer path: a learning rate of 1e30 overflows the next
+    batch loss and mlp_deep_check_errors reports MLP_ERR_NONFINITE once."""
+    h, L = 64, 2
+    d = datagen.make_data(1024, 32, epochs=1, seed=72)
+    P = _gauss_net(np.random.default_rng(72), h, L)
+    ctx, _ = _ctx(mlp, P, h, L, 256)
+    mlp.mlp_deep_train_epochs(ctx, _to(d.X), _to(d.Y), 256, 1e30, 1, perm=_to(d.perm))
+    with pytest.raises(mlp.MLPError) as e:
+        mlp.mlp_deep_check_errors(ctx)
+    assert e.value.status == -5
+    mlp.mlp_deep_check_errors(ctx)

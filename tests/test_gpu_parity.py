@@ -515,3 +515,25 @@ def test_workspace_reused_by_a_new_context(mlp):
                                 d.W2.astype(np.float64), idx, z, zabs, yp)
         assert rel(g1, r1a) <= 1e-4 and rel(dW2.cpu().numpy(), r2) <= 1e-4
         del ctx
+
+
+@pytest.mark.parametrize("strategy", [None, "tile", "optimized", "baseline"])
+def test_divergence_is_flagged(mlp, strategy):
+    """A learning rate of 1e30 sends the weights to ~1e30 after the first step,
+    so the next batch loss overflows: mlp_check_errors reports MLP_ERR_NONFINITE
+    (and clears it). A finite run afterwards raises nothing."""
+    d = datagen.make_data(2048, 256, epochs=1, shuffle=True, seed=71)
+    print("strategy", strategy, flush=True)
+    ctx, w1, w2 = _ctx(mlp, d.W1, d.W2, 256, strategy)
+    X, Y, P = _to(d.X), _to(d.Y), _to(d.perm)
+    mlp.mlp_train_epochs(ctx, X, Y, 256, 1e30, 1, perm=P)
+    with pytest.raises(mlp.MLPError) as e:
+        mlp.mlp_check_errors(ctx)
+    assert e.value.status == -5
+    mlp.mlp_check_errors(ctx)                       # the check cleared the flag
+    w1.copy_(_to(d.W1))
+    w2.copy_(_to(d.W2))
+    sl = torch.zeros(8, dtype=torch.float32, device="cuda")
+    mlp.mlp_train_epochs(ctx, X, Y, 256, 0.002, 1, perm=P, step_loss=sl)
+    mlp.mlp_check_errors(ctx)
+    assert np.all(np.isfinite(sl.cpu().numpy()))
