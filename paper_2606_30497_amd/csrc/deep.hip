@@ -46,9 +46,7 @@ namespace mlp {
 
 constexpr int GT = 64;        // GEMM tile (M and N)
 constexpr int GK = 32;        // K chunk
-constexpr int GLS = 80;       // LDS row stride of a k-major operand tile ([k][m], floats)
-constexpr int GMS = 34;       // LDS row stride of an m-major operand tile ([m][k], floats)
-constexpr int GLDS = GK * GLS;   // floats per operand tile (>= GT * GMS)
+constexpr int GMS = 34;       // LDS row stride of an x-major operand tile ([x][k], floats)
 constexpr int GSTAGES = 2;    // K chunks in flight (register stages; 3 or 4 measured slower)
 constexpr int GEMM_CUS = 256; // compute units the tile choice plans for
 constexpr int SPLIT_MAX = 64; // row chunks of a weight-gradient product
@@ -58,12 +56,12 @@ constexpr int DEEP_MAX_LAYERS = 8;
 enum { OP_NN = 0, OP_TN = 1, OP_NT = 2 };
 enum { EP_NONE = 0, EP_RELU = 1, EP_MASK = 2 };
 
-// Global -> register staging of one K chunk of a TM x 64 output tile: each of
-// the 256 threads holds TM / 32 float4 of the a tile ([TM x 32]) and two of the
-// b tile ([32 x 64]).
-template <int TM>
+// Global -> register staging of one K chunk of a TM x TN output tile: each of
+// the 256 threads holds TM / 32 float4 of the a tile ([TM x 32]) and TN / 32 of
+// the b tile ([32 x TN]).
+template <int TM, int TN>
 struct Stage {
-    float4 a[TM / 32], b[2];
+    float4 a[TM / 32], b[TN / 32];
 };
 
 // Sixteen zero bytes in device memory: a lane whose float4 lies outside its
@@ -80,125 +78,130 @@ __device__ __forceinline__ float4 ld4(bool ok, const float *p) {
     return *reinterpret_cast<const float4 *>(ok ? p : g_zero16);
 }
 
-// Thread t's float4 h of an a tile: loaded along m (k-major, TN) it is
-// (k, m) = (t / (TM/4) + (1024/TM) h, 4 (t % (TM/4))); loaded along k
-// (m-major) it is (m, k) = (t / (256/TM), 4 (t % (256/TM)) + (1024/TM) h).
-// The b tile is the TM = 64 case of the same maps with n for m.
-template <int OP, int TM>
-__device__ __forceinline__ void gemm_fetch(Stage<TM> &st, const float *__restrict__ A, int lda,
-                                           const float *__restrict__ B, int ldb, int64_t M, int N,
-                                           int64_t m0, int n0, int64_t k0, int64_t ke, int t) {
+// LDS row stride of a k-major operand tile of width T ([k][x], floats): T + 16,
+// so that the four k rows an MFMA operand read touches per wave fall in four
+// different groups of 16 banks.
+__host__ __device__ constexpr int kmajor_stride(int T) { return T + 16; }
+// floats of one LDS operand tile of width T (k-major [32][T + 16] or
+// x-major [T][GMS])
+__host__ __device__ constexpr int tile_floats(int T) {
+    return GK * kmajor_stride(T) > T * GMS ? GK * kmajor_stride(T) : T * GMS;
+}
+
+// One operand tile of width T (T = 32, 64 or 128; x is m for the a tile, n
+// for the b tile) and K chunk [k0, k0 + 32), thread t's float4 h (h < T / 32):
+//   loaded along x (k-major operand, P[k ld + x]):
+//     (k, x) = (t / (T/4) + (1024/T) h, 4 (t % (T/4)))
+//   loaded along k (x-major operand, P[x ld + k]):
+//     (x, k) = (t / (256/T), 4 (t % (256/T)) + (1024/T) h)
+template <bool KMAJOR, int T>
+__device__ __forceinline__ void fetch_operand(float4 (&r)[T / 32], const float *__restrict__ P,
+                                              int ld, int64_t xlim, int64_t x0, int64_t k0,
+                                              int64_t ke, int t) {
 #pragma unroll
-    for (int h = 0; h < TM / 32; ++h) {
-        if constexpr (OP == OP_TN) {              // a(m, k) = A[k lda + m]: float4 along m
-            const int64_t k = k0 + t / (TM / 4) + (1024 / TM) * h, m = m0 + (t % (TM / 4)) * 4;
-            st.a[h] = ld4(k < ke && m < M, A + k * lda + m);
-        } else {                                  // a(m, k) = A[m lda + k]: float4 along k
-            const int64_t m = m0 + t / (256 / TM), k = k0 + (t % (256 / TM)) * 4 + (1024 / TM) * h;
-            st.a[h] = ld4(m < M && k < ke, A + m * lda + k);
-        }
-    }
-#pragma unroll
-    for (int h = 0; h < 2; ++h) {
-        if constexpr (OP == OP_NT) {              // b(k, n) = B[n ldb + k]: float4 along k
-            const int64_t n = n0 + (t >> 2), k = k0 + (t & 3) * 4 + 16 * h;
-            st.b[h] = ld4(n < N && k < ke, B + n * ldb + k);
-        } else {                                  // b(k, n) = B[k ldb + n]: float4 along n
-            const int64_t k = k0 + (t >> 4) + 16 * h, n = n0 + (t & 15) * 4;
-            st.b[h] = ld4(k < ke && n < N, B + k * ldb + n);
+    for (int h = 0; h < T / 32; ++h) {
+        if constexpr (KMAJOR) {
+            const int64_t k = k0 + t / (T / 4) + (1024 / T) * h, x = x0 + (t % (T / 4)) * 4;
+            r[h] = ld4(k < ke && x < xlim, P + k * ld + x);
+        } else {
+            const int64_t x = x0 + t / (256 / T), k = k0 + (t % (256 / T)) * 4 + (1024 / T) * h;
+            r[h] = ld4(x < xlim && k < ke, P + x * ld + k);
         }
     }
 }
 
-// Registers -> LDS. An operand loaded along m (or n) is stored k-major
-// ([k][m], stride GLS); one loaded along k is stored as loaded, m-major
-// ([m][k], stride GMS = 34: the 16 m rows x 2 k columns an MFMA operand read
-// touches per half wave land in 32 distinct banks).
-template <int OP, int TM>
-__device__ __forceinline__ void gemm_stash(const Stage<TM> &st, float *As, float *Bs, int t) {
+// Registers -> LDS: a k-major operand is stored as loaded, [k][x] with stride
+// T + 16; an x-major one as loaded too, [x][k] with stride GMS = 34 (the 16 x
+// rows x 2 k columns an MFMA operand read touches per half wave land in 32
+// distinct banks), in 8-byte stores (the stride is not a multiple of 4).
+template <bool KMAJOR, int T>
+__device__ __forceinline__ void stash_operand(const float4 (&r)[T / 32], float *S, int t) {
 #pragma unroll
-    for (int h = 0; h < TM / 32; ++h) {
-        const float4 a = st.a[h];
-        if constexpr (OP == OP_TN) {
-            *reinterpret_cast<float4 *>(As + (t / (TM / 4) + (1024 / TM) * h) * GLS + (t % (TM / 4)) * 4) = a;
+    for (int h = 0; h < T / 32; ++h) {
+        if constexpr (KMAJOR) {
+            *reinterpret_cast<float4 *>(S + (t / (T / 4) + (1024 / T) * h) * kmajor_stride(T) +
+                                        (t % (T / 4)) * 4) = r[h];
         } else {
-            float2 *d = reinterpret_cast<float2 *>(As + (t / (256 / TM)) * GMS + (t % (256 / TM)) * 4 +
-                                                   (1024 / TM) * h);
-            d[0] = make_float2(a.x, a.y);
-            d[1] = make_float2(a.z, a.w);
+            float2 *d = reinterpret_cast<float2 *>(S + (t / (256 / T)) * GMS + (t % (256 / T)) * 4 +
+                                                   (1024 / T) * h);
+            d[0] = make_float2(r[h].x, r[h].y);
+            d[1] = make_float2(r[h].z, r[h].w);
         }
     }
-#pragma unroll
-    for (int h = 0; h < 2; ++h) {
-        const float4 b = st.b[h];
-        if constexpr (OP == OP_NT) {
-            float2 *d = reinterpret_cast<float2 *>(Bs + (t >> 2) * GMS + (t & 3) * 4 + 16 * h);
-            d[0] = make_float2(b.x, b.y);
-            d[1] = make_float2(b.z, b.w);
-        } else {
-            *reinterpret_cast<float4 *>(Bs + ((t >> 4) + 16 * h) * GLS + (t & 15) * 4) = b;
-        }
-    }
+}
+
+template <int OP, int TM, int TN>
+__device__ __forceinline__ void gemm_fetch(Stage<TM, TN> &st, const float *__restrict__ A, int lda,
+                                           const float *__restrict__ B, int ldb, int64_t M, int N,
+                                           int64_t m0, int n0, int64_t k0, int64_t ke, int t) {
+    fetch_operand<OP == OP_TN, TM>(st.a, A, lda, M, m0, k0, ke, t);   // TN: a(m, k) = A[k lda + m]
+    fetch_operand<OP != OP_NT, TN>(st.b, B, ldb, N, n0, k0, ke, t);   // NT: b(k, n) = B[n ldb + k]
+}
+
+template <int OP, int TM, int TN>
+__device__ __forceinline__ void gemm_stash(const Stage<TM, TN> &st, float *As, float *Bs, int t) {
+    stash_operand<OP == OP_TN, TM>(st.a, As, t);
+    stash_operand<OP != OP_NT, TN>(st.b, Bs, t);
 }
 
 // C[m][n] = sum_k a(m, k) b(k, n) over k in [k_begin(z), k_end(z)), where
 //   NN: a(m, k) = A[m lda + k],  b(k, n) = B[k ldb + n]
 //   TN: a(m, k) = A[k lda + m],  b(k, n) = B[k ldb + n]
 //   NT: a(m, k) = A[m lda + k],  b(k, n) = B[n ldb + k]
-// Output tile TM x 64 (TM = 64 or 32; each of the four waves computes a
-// TM/2 x 32 quarter). Grid: (ceil(M/TM), ceil(N/64), splits); split z covers k
-// in [z kc, min(K, z kc + kc))
-// and writes C + z * c_split. N and the contiguous dimension of every operand
-// are multiples of 16 (hidden widths and d_in); M and K are arbitrary. The next
-// two K chunks are loaded into registers while the current one is on the matrix
-// cores.
-template <int OP, int EP, int TM>
+// Output tile TM x TN (launched as 32 x 64 or 64 x 64); each of the four waves
+// computes a TM/2 x TN/2 quarter as (TM/32) x (TN/32) MFMA tiles of 16 x 16.
+// Grid: (ceil(M/TM), ceil(N/TN), splits); split z covers k in [z kc, min(K,
+// z kc + kc)) and writes C + z * c_split. N and the contiguous dimension of
+// every operand are multiples of 16 (hidden widths and d_in); M and K are
+// arbitrary.
+template <int OP, int EP, int TM, int TN>
 __global__ __launch_bounds__(256) void k_gemm(const float *__restrict__ A, int lda,
                                               const float *__restrict__ B, int ldb,
                                               float *__restrict__ C, int ldc, int64_t c_split,
                                               int64_t M, int N, int64_t K, int64_t kc,
                                               const float *__restrict__ G, int ldg) {
-    __shared__ __attribute__((aligned(16))) float As2[2][GLDS];
-    __shared__ __attribute__((aligned(16))) float Bs2[2][GLDS];
+    constexpr int MI = TM / 32, NJ = TN / 32;   // 16 x 16 MFMA tiles per wave
+    constexpr int AS = kmajor_stride(TM), BS = kmajor_stride(TN);
+    __shared__ __attribute__((aligned(16))) float As2[2][tile_floats(TM)];
+    __shared__ __attribute__((aligned(16))) float Bs2[2][tile_floats(TN)];
     const int t = threadIdx.x;
     const int lane = t & 63, wave = t >> 6;
     const int li = lane & 15, lq = lane >> 4;
     const int wm = wave >> 1, wn = wave & 1;
-    constexpr int MI = TM / 32;   // 16-row MFMA tiles per wave
     const int64_t m0 = (int64_t)blockIdx.x * TM;
-    const int n0 = blockIdx.y * GT;
+    const int n0 = blockIdx.y * TN;
     const int64_t kb = (int64_t)blockIdx.z * kc;
     const int64_t ke = kb + kc < K ? kb + kc : K;
 
-    f4 acc[MI][2];
+    f4 acc[MI][NJ];
 #pragma unroll
     for (int i = 0; i < MI; ++i)
 #pragma unroll
-        for (int j = 0; j < 2; ++j) acc[i][j] = f4{0.f, 0.f, 0.f, 0.f};
+        for (int j = 0; j < NJ; ++j) acc[i][j] = f4{0.f, 0.f, 0.f, 0.f};
 
-    // NS chunks in flight: chunk c + NS is fetched into the registers
-    // chunk c has just left, while chunk c is on the matrix cores. Chunks
-    // alternate between two LDS buffers, so one barrier per chunk suffices: the
-    // buffer a chunk is written to was last read by the chunk before the
-    // previous barrier, which every wave has passed. Every pass of
-    // the main loop issues the same loads (the fetches past the last chunk read
-    // the zero block and are never stashed), so the compiler can wait for each
-    // stage's own loads only, not for all loads in flight.
+    // NS chunks in flight: chunk c + NS is fetched into the registers chunk c
+    // has just left, while chunk c is on the matrix cores. Chunks alternate
+    // between two LDS buffers, so one barrier per chunk suffices: the buffer a
+    // chunk is written to was last read by the chunk before the previous
+    // barrier, which every wave has passed. Every pass of the main loop issues
+    // the same loads (the fetches past the last chunk read the zero block and
+    // are never stashed), so the compiler can wait for each stage's own loads
+    // only, not for all loads in flight.
     constexpr int NS = GSTAGES;
     const int64_t nch = (ke - kb + GK - 1) / GK;
-    Stage<TM> st[NS];
+    Stage<TM, TN> st[NS];
 #pragma unroll
     for (int q = 0; q < NS; ++q)
-        gemm_fetch<OP, TM>(st[q], A, lda, B, ldb, M, N, m0, n0, kb + q * GK, ke, t);
+        gemm_fetch<OP, TM, TN>(st[q], A, lda, B, ldb, M, N, m0, n0, kb + q * GK, ke, t);
     // the mask of the epilogue, loaded now (clamped addresses, no lane condition)
     // so that its loads overlap the K loop instead of each waiting at the end
-    float gm[MI][2][4];
+    float gm[EP == EP_MASK ? MI : 1][EP == EP_MASK ? NJ : 1][4];
     if constexpr (EP == EP_MASK) {
 #pragma unroll
         for (int i = 0; i < MI; ++i)
 #pragma unroll
-            for (int j = 0; j < 2; ++j) {
-                const int n = n0 + wn * 32 + j * 16 + li;
+            for (int j = 0; j < NJ; ++j) {
+                const int n = n0 + wn * (TN / 2) + j * 16 + li;
                 const int nc = n < N ? n : N - 1;
 #pragma unroll
                 for (int v = 0; v < 4; ++v) {
@@ -213,21 +216,21 @@ __global__ __launch_bounds__(256) void k_gemm(const float *__restrict__ A, int l
 #pragma unroll
         for (int ks = 0; ks < GK / 4; ++ks) {
             const int kr = ks * 4 + lq;
-            float a[MI], b[2];
+            float a[MI], b[NJ];
 #pragma unroll
             for (int i = 0; i < MI; ++i) {
                 const int m = wm * (TM / 2) + i * 16 + li;
-                a[i] = OP == OP_TN ? As[kr * GLS + m] : As[m * GMS + kr];
+                a[i] = OP == OP_TN ? As[kr * AS + m] : As[m * GMS + kr];
             }
 #pragma unroll
-            for (int j = 0; j < 2; ++j) {
-                const int n = wn * 32 + j * 16 + li;
-                b[j] = OP == OP_NT ? Bs[n * GMS + kr] : Bs[kr * GLS + n];
+            for (int j = 0; j < NJ; ++j) {
+                const int n = wn * (TN / 2) + j * 16 + li;
+                b[j] = OP == OP_NT ? Bs[n * GMS + kr] : Bs[kr * BS + n];
             }
 #pragma unroll
             for (int i = 0; i < MI; ++i)
 #pragma unroll
-                for (int j = 0; j < 2; ++j)
+                for (int j = 0; j < NJ; ++j)
                     acc[i][j] = __builtin_amdgcn_mfma_f32_16x16x4f32(a[i], b[j], acc[i][j], 0, 0, 0);
         }
     };
@@ -236,9 +239,9 @@ __global__ __launch_bounds__(256) void k_gemm(const float *__restrict__ A, int l
 #pragma unroll
         for (int q = 0; q < NS; ++q) {
             const int buf = (int)((c + q) & 1);
-            gemm_stash<OP, TM>(st[q], As2[buf], Bs2[buf], t);
+            gemm_stash<OP, TM, TN>(st[q], As2[buf], Bs2[buf], t);
             __syncthreads();
-            gemm_fetch<OP, TM>(st[q], A, lda, B, ldb, M, N, m0, n0, kb + (c + q + NS) * GK, ke, t);
+            gemm_fetch<OP, TM, TN>(st[q], A, lda, B, ldb, M, N, m0, n0, kb + (c + q + NS) * GK, ke, t);
             mfma_chunk(buf);
         }
     }
@@ -247,7 +250,7 @@ __global__ __launch_bounds__(256) void k_gemm(const float *__restrict__ A, int l
     for (int q = 0; q < NS - 1; ++q) {
         if (c + q < nch) {
             const int buf = (int)((c + q) & 1);
-            gemm_stash<OP, TM>(st[q], As2[buf], Bs2[buf], t);
+            gemm_stash<OP, TM, TN>(st[q], As2[buf], Bs2[buf], t);
             __syncthreads();
             mfma_chunk(buf);
         }
@@ -257,8 +260,8 @@ __global__ __launch_bounds__(256) void k_gemm(const float *__restrict__ A, int l
 #pragma unroll
     for (int i = 0; i < MI; ++i)
 #pragma unroll
-        for (int j = 0; j < 2; ++j) {
-            const int n = n0 + wn * 32 + j * 16 + li;
+        for (int j = 0; j < NJ; ++j) {
+            const int n = n0 + wn * (TN / 2) + j * 16 + li;
 #pragma unroll
             for (int v = 0; v < 4; ++v) {
                 const int64_t m = m0 + wm * (TM / 2) + i * 16 + 4 * lq + v;
@@ -549,9 +552,11 @@ static size_t deep_ws_floats(int h, int L, int64_t mb) {
            (size_t)(L + 2) * pad64f(b * (size_t)h) + (size_t)part_floats(h, L, mb);
 }
 
-// 32-row tiles when 64-row ones would leave fewer than two workgroups per CU
-// (the 256-wide layers: one 64 x 64 tile per CU leaves one wave per SIMD), or
-// when M itself is 32 (the weight gradient of W_1).
+// Tile choice: 64 x 64, or 32 x 64 where 64-row tiles would leave fewer than
+// two workgroups per CU (the 256-wide layers) or M itself is 32 (the weight
+// gradient of W_1). Larger tiles (128 x 64, 128 x 128) halve the operand
+// traffic per MFMA but leave one or two workgroups per CU on the 1024-wide
+// products, which measured 6-8 % slower than four.
 template <int OP, int EP>
 static hipError_t gemm(hipStream_t st, const float *A, int lda, const float *B, int ldb, float *C,
                        int ldc, int64_t c_split, int64_t M, int N, int64_t K, int splits,
@@ -561,10 +566,10 @@ static hipError_t gemm(hipStream_t st, const float *A, int lda, const float *B, 
     const int tm = small ? 32 : GT;
     const dim3 grid((unsigned)((M + tm - 1) / tm), (unsigned)((N + GT - 1) / GT), (unsigned)splits);
     if (small)
-        hipLaunchKernelGGL((k_gemm<OP, EP, 32>), grid, dim3(256), 0, st, A, lda, B, ldb, C, ldc,
+        hipLaunchKernelGGL((k_gemm<OP, EP, 32, GT>), grid, dim3(256), 0, st, A, lda, B, ldb, C, ldc,
                            c_split, M, N, K, kc, G, ldg);
     else
-        hipLaunchKernelGGL((k_gemm<OP, EP, GT>), grid, dim3(256), 0, st, A, lda, B, ldb, C, ldc,
+        hipLaunchKernelGGL((k_gemm<OP, EP, GT, GT>), grid, dim3(256), 0, st, A, lda, B, ldb, C, ldc,
                            c_split, M, N, K, kc, G, ldg);
     return hipGetLastError();
 }
