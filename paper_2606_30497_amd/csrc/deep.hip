@@ -17,6 +17,9 @@
 //   k_gemm<TN, NONE>   dW_l = H_{l-1}^T G_l, split over row chunks (grid z);
 //                      each chunk writes its own partial, summed in chunk order
 //   k_gemm<NT, MASK>   G_{l-1} = (G_l W_l^T) masked by H_{l-1} > 0
+//   k_gemm_pair        the weight gradient and the back-propagation of one
+//                      layer (both read G_l, neither reads the other's output)
+//                      in one launch
 //   k_deep_out         Ypred, residual, dZ_o, G_L and the dw_o partial of a
 //                      chunk of rows (one wave per row)
 //   k_deep_apply       sums every gradient's chunk partials in order and
@@ -25,12 +28,13 @@
 // Every output element is one lane's sum in a fixed order, so results are
 // bitwise reproducible.
 //
-// GEMM tile: 64 x 64 outputs per workgroup of four waves (each 32 x 32, 2 x 2
-// v_mfma_f32_16x16x4f32 tiles), K in chunks of 32 staged in LDS k-major with a
-// row stride of 80 floats (k-major) or 34 (m-major), so that MFMA operand reads
-// are conflict-free, alternating between two LDS buffers (one barrier per
-// chunk); the next two chunks' global loads are in flight while the current
-// chunk is computed.
+// GEMM tile: 64 x 64 (or 32 x 64) outputs per workgroup of four waves (each a
+// quarter, as 16 x 16 v_mfma_f32_16x16x4f32 tiles), K in chunks of 32 staged in
+// LDS (operands read along m or n stored k-major with a row stride of TM + 16
+// floats, operands read along k as loaded with a stride of 34, so that MFMA
+// operand reads are conflict-free), alternating between two LDS buffers (one
+// barrier per chunk); the next two chunks' global loads are in flight while the
+// current chunk is computed.
 #include <hip/hip_runtime.h>
 
 #include <math.h>
@@ -154,23 +158,46 @@ __device__ __forceinline__ void gemm_stash(const Stage<TM, TN> &st, float *As, f
 // z kc + kc)) and writes C + z * c_split. N and the contiguous dimension of
 // every operand are multiples of 16 (hidden widths and d_in); M and K are
 // arbitrary.
+struct GemmArgs {
+    const float *A;
+    int lda;
+    const float *B;
+    int ldb;
+    float *C;
+    int ldc;
+    int64_t c_split, M;
+    int N;
+    int64_t K, kc;
+    const float *G;   // mask operand of the MASK epilogue
+    int ldg;
+    int gx, gy, gz;   // grid of this product, in tiles
+};
+
+// LDS floats of one workgroup of a TM x TN product (two buffers of each operand)
+__host__ __device__ constexpr int gemm_lds_floats(int TM, int TN) {
+    return 2 * (tile_floats(TM) + tile_floats(TN));
+}
+
+// One output tile (bx, by) of split bz; lds holds gemm_lds_floats(TM, TN).
 template <int OP, int EP, int TM, int TN>
-__global__ __launch_bounds__(256) void k_gemm(const float *__restrict__ A, int lda,
-                                              const float *__restrict__ B, int ldb,
-                                              float *__restrict__ C, int ldc, int64_t c_split,
-                                              int64_t M, int N, int64_t K, int64_t kc,
-                                              const float *__restrict__ G, int ldg) {
+__device__ __forceinline__ void gemm_block(const GemmArgs &g, int bx, int by, int bz,
+                                           float *__restrict__ lds) {
     constexpr int MI = TM / 32, NJ = TN / 32;   // 16 x 16 MFMA tiles per wave
     constexpr int AS = kmajor_stride(TM), BS = kmajor_stride(TN);
-    __shared__ __attribute__((aligned(16))) float As2[2][tile_floats(TM)];
-    __shared__ __attribute__((aligned(16))) float Bs2[2][tile_floats(TN)];
+    float *As2[2] = {lds, lds + tile_floats(TM)};
+    float *Bs2[2] = {lds + 2 * tile_floats(TM), lds + 2 * tile_floats(TM) + tile_floats(TN)};
+    const float *__restrict__ A = g.A;
+    const float *__restrict__ B = g.B;
+    const float *__restrict__ G = g.G;
+    const int lda = g.lda, ldb = g.ldb, ldg = g.ldg, ldc = g.ldc, N = g.N;
+    const int64_t M = g.M, K = g.K, kc = g.kc;
     const int t = threadIdx.x;
     const int lane = t & 63, wave = t >> 6;
     const int li = lane & 15, lq = lane >> 4;
     const int wm = wave >> 1, wn = wave & 1;
-    const int64_t m0 = (int64_t)blockIdx.x * TM;
-    const int n0 = blockIdx.y * TN;
-    const int64_t kb = (int64_t)blockIdx.z * kc;
+    const int64_t m0 = (int64_t)bx * TM;
+    const int n0 = by * TN;
+    const int64_t kb = (int64_t)bz * kc;
     const int64_t ke = kb + kc < K ? kb + kc : K;
 
     f4 acc[MI][NJ];
@@ -256,7 +283,7 @@ __global__ __launch_bounds__(256) void k_gemm(const float *__restrict__ A, int l
         }
     }
     // ---- epilogue: lane holds C[4 lq + v][li] of each 16 x 16 tile ----
-    float *Cz = C + (int64_t)blockIdx.z * c_split;
+    float *Cz = g.C + (int64_t)bz * g.c_split;
 #pragma unroll
     for (int i = 0; i < MI; ++i)
 #pragma unroll
@@ -272,6 +299,29 @@ __global__ __launch_bounds__(256) void k_gemm(const float *__restrict__ A, int l
                 Cz[m * ldc + n] = r;
             }
         }
+}
+
+template <int OP, int EP, int TM, int TN>
+__global__ __launch_bounds__(256) void k_gemm(const GemmArgs g) {
+    __shared__ __attribute__((aligned(16))) float lds[gemm_lds_floats(TM, TN)];
+    gemm_block<OP, EP, TM, TN>(g, blockIdx.x, blockIdx.y, blockIdx.z, lds);
+}
+
+// Two independent products in one launch (a one-dimensional grid): blocks
+// [0, g1.gx g1.gy g1.gz) compute the first, the rest the second. With both
+// resident together the CUs hold twice the workgroups of either alone.
+template <int OP1, int EP1, int TM1, int TN1, int OP2, int EP2, int TM2, int TN2>
+__global__ __launch_bounds__(256) void k_gemm_pair(const GemmArgs g1, const GemmArgs g2) {
+    constexpr int L1 = gemm_lds_floats(TM1, TN1), L2 = gemm_lds_floats(TM2, TN2);
+    __shared__ __attribute__((aligned(16))) float lds[L1 > L2 ? L1 : L2];
+    const int n1 = g1.gx * g1.gy * g1.gz;
+    int b = blockIdx.x;
+    if (b < n1) {
+        gemm_block<OP1, EP1, TM1, TN1>(g1, b % g1.gx, (b / g1.gx) % g1.gy, b / (g1.gx * g1.gy), lds);
+    } else {
+        b -= n1;
+        gemm_block<OP2, EP2, TM2, TN2>(g2, b % g2.gx, (b / g2.gx) % g2.gy, b / (g2.gx * g2.gy), lds);
+    }
 }
 
 // Xb[t][k] = X[r_t][k], Yb[t] = Y[r_t], r_t = idx[off + t] (or off + t);
@@ -557,20 +607,59 @@ static size_t deep_ws_floats(int h, int L, int64_t mb) {
 // gradient of W_1). Larger tiles (128 x 64, 128 x 128) halve the operand
 // traffic per MFMA but leave one or two workgroups per CU on the 1024-wide
 // products, which measured 6-8 % slower than four.
+static GemmArgs gemm_args(const float *A, int lda, const float *B, int ldb, float *C, int ldc,
+                          int64_t c_split, int64_t M, int N, int64_t K, int splits, int64_t kc,
+                          const float *G, int ldg, bool *small) {
+    const int64_t tiles64 = ((M + GT - 1) / GT) * ((N + GT - 1) / GT) * splits;
+    *small = M <= 32 || tiles64 < 2 * GEMM_CUS;
+    const int tm = *small ? 32 : GT;
+    GemmArgs g;
+    g.A = A;
+    g.lda = lda;
+    g.B = B;
+    g.ldb = ldb;
+    g.C = C;
+    g.ldc = ldc;
+    g.c_split = c_split;
+    g.M = M;
+    g.N = N;
+    g.K = K;
+    g.kc = kc;
+    g.G = G;
+    g.ldg = ldg;
+    g.gx = (int)((M + tm - 1) / tm);
+    g.gy = (N + GT - 1) / GT;
+    g.gz = splits;
+    return g;
+}
+
 template <int OP, int EP>
 static hipError_t gemm(hipStream_t st, const float *A, int lda, const float *B, int ldb, float *C,
                        int ldc, int64_t c_split, int64_t M, int N, int64_t K, int splits,
                        int64_t kc, const float *G = nullptr, int ldg = 0) {
-    const int64_t tiles64 = ((M + GT - 1) / GT) * ((N + GT - 1) / GT) * splits;
-    const bool small = M <= 32 || tiles64 < 2 * GEMM_CUS;
-    const int tm = small ? 32 : GT;
-    const dim3 grid((unsigned)((M + tm - 1) / tm), (unsigned)((N + GT - 1) / GT), (unsigned)splits);
+    bool small;
+    const GemmArgs g = gemm_args(A, lda, B, ldb, C, ldc, c_split, M, N, K, splits, kc, G, ldg, &small);
+    const dim3 grid((unsigned)g.gx, (unsigned)g.gy, (unsigned)g.gz);
     if (small)
-        hipLaunchKernelGGL((k_gemm<OP, EP, 32, GT>), grid, dim3(256), 0, st, A, lda, B, ldb, C, ldc,
-                           c_split, M, N, K, kc, G, ldg);
+        hipLaunchKernelGGL((k_gemm<OP, EP, 32, GT>), grid, dim3(256), 0, st, g);
     else
-        hipLaunchKernelGGL((k_gemm<OP, EP, GT, GT>), grid, dim3(256), 0, st, A, lda, B, ldb, C, ldc,
-                           c_split, M, N, K, kc, G, ldg);
+        hipLaunchKernelGGL((k_gemm<OP, EP, GT, GT>), grid, dim3(256), 0, st, g);
+    return hipGetLastError();
+}
+
+// The two independent products g1 (OP1, EP1) and g2 (OP2, EP2) in one launch.
+template <int OP1, int EP1, int OP2, int EP2>
+static hipError_t gemm_pair(hipStream_t st, const GemmArgs &g1, bool small1, const GemmArgs &g2,
+                            bool small2) {
+    const dim3 grid((unsigned)(g1.gx * g1.gy * g1.gz + g2.gx * g2.gy * g2.gz));
+    if (small1 && small2)
+        hipLaunchKernelGGL((k_gemm_pair<OP1, EP1, 32, GT, OP2, EP2, 32, GT>), grid, dim3(256), 0, st, g1, g2);
+    else if (small1)
+        hipLaunchKernelGGL((k_gemm_pair<OP1, EP1, 32, GT, OP2, EP2, GT, GT>), grid, dim3(256), 0, st, g1, g2);
+    else if (small2)
+        hipLaunchKernelGGL((k_gemm_pair<OP1, EP1, GT, GT, OP2, EP2, 32, GT>), grid, dim3(256), 0, st, g1, g2);
+    else
+        hipLaunchKernelGGL((k_gemm_pair<OP1, EP1, GT, GT, OP2, EP2, GT, GT>), grid, dim3(256), 0, st, g1, g2);
     return hipGetLastError();
 }
 
@@ -637,13 +726,21 @@ static hipError_t deep_step(DeepCtx &c, const float *X, int64_t n_rows, const fl
         const int K = l == 1 ? D_IN : h;
         const float *Hin = l == 1 ? c.Xb : c.H + (int64_t)(l - 2) * mbh;
         // dW_l = H_{l-1}^T G_l, eq. 18, split over row chunks
-        DEEP_TRY((gemm<OP_TN, EP_NONE>(c.stream, Hin, K, c.G[cur], h, c.part + sp.part_off[l - 1], h,
-                                       (int64_t)K * h, K, h, nb, sp.splits[l - 1], sp.kc[l - 1])));
+        bool s1, s2;
+        const GemmArgs gw = gemm_args(Hin, K, c.G[cur], h, c.part + sp.part_off[l - 1], h,
+                                      (int64_t)K * h, K, h, nb, sp.splits[l - 1], sp.kc[l - 1],
+                                      nullptr, 0, &s1);
         if (l > 1) {
-            // G_{l-1} = (G_l W_l^T) (.) [H_{l-1} > 0], eq. 17 one layer down
-            DEEP_TRY((gemm<OP_NT, EP_MASK>(c.stream, c.G[cur], h, c.params + layer_offset(h, l), h,
-                                           c.G[cur ^ 1], h, 0, nb, h, h, 1, h, Hin, h)));
+            // G_{l-1} = (G_l W_l^T) (.) [H_{l-1} > 0], eq. 17 one layer down; it
+            // reads G_l as the weight gradient does and writes the other buffer,
+            // so the two products share one launch
+            const GemmArgs gg = gemm_args(c.G[cur], h, c.params + layer_offset(h, l), h, c.G[cur ^ 1], h,
+                                          0, nb, h, h, 1, h, Hin, h, &s2);
+            DEEP_TRY((gemm_pair<OP_TN, EP_NONE, OP_NT, EP_MASK>(c.stream, gw, s1, gg, s2)));
             cur ^= 1;
+        } else {
+            DEEP_TRY((gemm<OP_TN, EP_NONE>(c.stream, Hin, K, c.G[cur], h, c.part + sp.part_off[l - 1], h,
+                                           (int64_t)K * h, K, h, nb, sp.splits[l - 1], sp.kc[l - 1])));
         }
     }
     // every gradient's partials summed and applied; the last workgroup takes the loss
