@@ -23,8 +23,9 @@
 //   k_deep_out         Ypred, residual, dZ_o, G_L and the dw_o partial of a
 //                      chunk of rows (one wave per row)
 //   k_deep_apply       sums every gradient's chunk partials in order and
-//                      applies eq. 19 (or writes the gradients); its last
-//                      workgroup reduces the batch loss in a fixed tree
+//                      applies eq. 19 (or writes the gradients); one workgroup
+//                      reduces the batch loss in a fixed tree, and in a training
+//                      loop the last ones gather the next step's rows
 // Every output element is one lane's sum in a fixed order, so results are
 // bitwise reproducible.
 //
@@ -326,23 +327,32 @@ __global__ __launch_bounds__(256) void k_gemm_pair(const GemmArgs g1, const Gemm
 
 // Xb[t][k] = X[r_t][k], Yb[t] = Y[r_t], r_t = idx[off + t] (or off + t);
 // out-of-range rows read row 0 and raise the sticky error.
-__global__ __launch_bounds__(256) void k_deep_gather(const float *__restrict__ X,
-                                                     const float *__restrict__ Y, int64_t n_rows,
-                                                     const int32_t *__restrict__ idx, int64_t off,
-                                                     int64_t nb, float *__restrict__ Xb,
-                                                     float *__restrict__ Yb, int32_t *err) {
-    const int64_t e = (int64_t)blockIdx.x * 256 + threadIdx.x;
-    if (e >= nb * (D_IN / 4)) return;
+struct GatherArgs {
+    const float *X, *Y;
+    int64_t n_rows;
+    const int32_t *idx;
+    int64_t off, nb;
+    float *Xb, *Yb;
+    int32_t *err;
+};
+
+// Element e of the gather: float4 e % 8 of batch row e / 8.
+__device__ __forceinline__ void gather_one(const GatherArgs &g, int64_t e) {
+    if (e >= g.nb * (D_IN / 4)) return;
     const int64_t t = e / (D_IN / 4);
     const int q = (int)(e % (D_IN / 4));
-    int64_t r = idx ? (int64_t)idx[off + t] : off + t;
-    if (r < 0 || r >= n_rows) {
-        __hip_atomic_store(err, (int32_t)MLP_ERR_INDEX, __ATOMIC_RELAXED, __HIP_MEMORY_SCOPE_AGENT);
+    int64_t r = g.idx ? (int64_t)g.idx[g.off + t] : g.off + t;
+    if (r < 0 || r >= g.n_rows) {
+        __hip_atomic_store(g.err, (int32_t)MLP_ERR_INDEX, __ATOMIC_RELAXED, __HIP_MEMORY_SCOPE_AGENT);
         r = 0;
     }
-    reinterpret_cast<float4 *>(Xb)[t * (D_IN / 4) + q] =
-        reinterpret_cast<const float4 *>(X)[r * (D_IN / 4) + q];
-    if (q == 0) Yb[t] = Y ? Y[r] : 0.0f;
+    reinterpret_cast<float4 *>(g.Xb)[t * (D_IN / 4) + q] =
+        reinterpret_cast<const float4 *>(g.X)[r * (D_IN / 4) + q];
+    if (q == 0) g.Yb[t] = g.Y ? g.Y[r] : 0.0f;
+}
+
+__global__ __launch_bounds__(256) void k_deep_gather(const GatherArgs g) {
+    gather_one(g, (int64_t)blockIdx.x * 256 + threadIdx.x);
 }
 
 // Forward output, one wave per row: Ypred = H_L w_o (eq. 13).
@@ -434,16 +444,22 @@ struct SplitPlan {
 };
 
 // Sum the chunk partials of every parameter's gradient in chunk order, then
-// eq. 19 (sgd) or write the gradient. The last workgroup reduces the batch loss
-// instead (eq. 14): thread i sums rows i, i + 256, ..., then a fixed binary
-// tree; step and epoch loss as in the one-layer paths.
+// eq. 19 (sgd) or write the gradient: workgroups [0, napply). Workgroup napply
+// reduces the batch loss instead (eq. 14): thread i sums rows i, i + 256, ...,
+// then a fixed binary tree; step and epoch loss as in the one-layer paths. The
+// workgroups after it gather the next training step's rows (the gathered
+// buffers' last readers, the W_1 gradient and the output kernel, ran before).
 __global__ __launch_bounds__(256) void k_deep_apply(const float *__restrict__ part, SplitPlan sp,
-                                                    int64_t np, float *__restrict__ params,
+                                                    int64_t np, int napply, float *__restrict__ params,
                                                     float *__restrict__ dparams, float lr, int sgd,
                                                     const float *__restrict__ sq, int64_t nb,
-                                                    ReduceArgs ra) {
+                                                    ReduceArgs ra, const GatherArgs next) {
     constexpr int U = 32;     // loads in flight per lane; the adds stay in index order
-    if (blockIdx.x == gridDim.x - 1) {
+    if ((int)blockIdx.x > napply) {
+        gather_one(next, (int64_t)(blockIdx.x - napply - 1) * 256 + threadIdx.x);
+        return;
+    }
+    if ((int)blockIdx.x == napply) {
         __shared__ float red[256];
         const int i = threadIdx.x;
         float v = 0.0f;
@@ -705,15 +721,35 @@ static hipError_t launch_out(const DeepCtx &c, const float *HL, const float *wo,
     return hipErrorInvalidValue;
 }
 
+static GatherArgs gather_args(const DeepCtx &c, const float *X, const float *Y, int64_t n_rows,
+                              const int32_t *idx, int64_t off, int64_t nb) {
+    GatherArgs g;
+    g.X = X;
+    g.Y = Y;
+    g.n_rows = n_rows;
+    g.idx = idx;
+    g.off = off;
+    g.nb = nb;
+    g.Xb = c.Xb;
+    g.Yb = c.Yb;
+    g.err = &c.ctl->err;
+    return g;
+}
+
 // One step (or one gradient evaluation) on batch rows [off, off + nb) of idx.
+// With gathered, the rows are already in Xb / Yb (gathered by the previous
+// step's update kernel); with next, the update kernel also gathers the rows of
+// the next step.
 static hipError_t deep_step(DeepCtx &c, const float *X, int64_t n_rows, const float *Y,
                             const int32_t *idx, int64_t off, int64_t nb, const ReduceArgs &ra,
-                            float *dparams) {
+                            float *dparams, bool gathered = false, const GatherArgs *next = nullptr) {
     const int h = c.hidden, L = c.layers;
     const int64_t mbh = c.max_batch * h;
-    hipLaunchKernelGGL(k_deep_gather, dim3(blocks_of(nb * (D_IN / 4), 256)), dim3(256), 0, c.stream,
-                       X, Y, n_rows, idx, off, nb, c.Xb, c.Yb, &c.ctl->err);
-    DEEP_TRY(hipGetLastError());
+    if (!gathered) {
+        hipLaunchKernelGGL(k_deep_gather, dim3(blocks_of(nb * (D_IN / 4), 256)), dim3(256), 0,
+                           c.stream, gather_args(c, X, Y, n_rows, idx, off, nb));
+        DEEP_TRY(hipGetLastError());
+    }
     DEEP_TRY(deep_forward_layers(c, nb));
     const float *HL = c.H + (int64_t)(L - 1) * mbh;
     const float *wo = c.params + layer_offset(h, L + 1);
@@ -744,8 +780,13 @@ static hipError_t deep_step(DeepCtx &c, const float *X, int64_t n_rows, const fl
         }
     }
     // every gradient's partials summed and applied; the last workgroup takes the loss
-    hipLaunchKernelGGL(k_deep_apply, dim3(blocks_of(c.np, 256) + 1), dim3(256), 0, c.stream, c.part,
-                       sp, c.np, c.params, dparams, ra.lr, ra.sgd, c.sq, nb, ra);
+    const unsigned napply = blocks_of(c.np, 256);
+    GatherArgs none;
+    memset(&none, 0, sizeof(none));
+    const unsigned ng = next ? blocks_of(next->nb * (D_IN / 4), 256) : 0;
+    hipLaunchKernelGGL(k_deep_apply, dim3(napply + 1 + ng), dim3(256), 0, c.stream, c.part, sp,
+                       c.np, (int)napply, c.params, dparams, ra.lr, ra.sgd, c.sq, nb, ra,
+                       next ? *next : none);
     return hipGetLastError();
 }
 
@@ -829,7 +870,7 @@ extern "C" mlp_status mlp_deep_forward(mlp_deep_t c, const float *X, int64_t n_r
     for (int64_t off = 0; off < B; off += c->max_batch) {
         const int64_t nb = B - off < c->max_batch ? B - off : c->max_batch;
         hipLaunchKernelGGL(k_deep_gather, dim3(blocks_of(nb * (D_IN / 4), 256)), dim3(256), 0,
-                           c->stream, X, nullptr, n_rows, idx, off, nb, c->Xb, c->Yb, &c->ctl->err);
+                           c->stream, gather_args(*c, X, nullptr, n_rows, idx, off, nb));
         if (hipGetLastError() != hipSuccess) return MLP_ERR_HIP;
         if (deep_forward_layers(*c, nb) != hipSuccess) return MLP_ERR_HIP;
         hipLaunchKernelGGL(k_deep_ypred, dim3(blocks_of(nb, 4)), dim3(256), 0, c->stream, HL, h, wo,
@@ -901,11 +942,12 @@ extern "C" mlp_status mlp_deep_train_epochs(mlp_deep_t c, const float *X, const 
     if (epoch_loss) e = fill(tmp, epoch_loss, epochs, 0.0f);
     if (e != hipSuccess) return MLP_ERR_HIP;
     const int64_t spe = (n + batch - 1) / batch;
+    const int64_t total = max_steps >= 0 && max_steps < spe * epochs ? max_steps : spe * epochs;
     int64_t step = 0;
     deep_prof(c, true);
     for (int32_t ep = 0; ep < epochs && e == hipSuccess; ++ep) {
         for (int64_t s = 0; s < spe; ++s) {
-            if (max_steps >= 0 && step >= max_steps) break;
+            if (step >= total) break;
             const int64_t off = s * batch;
             const int64_t nb = n - off < batch ? n - off : batch;
             ReduceArgs a = deep_args(c, nb);
@@ -918,7 +960,17 @@ extern "C" mlp_status mlp_deep_train_epochs(mlp_deep_t c, const float *X, const 
             a.epoch = ep;
             a.first_in_epoch = s == 0;
             const int32_t *ix = perm ? perm + (int64_t)ep * n : nullptr;
-            e = deep_step(*c, X, n, Y, ix, off, nb, a, nullptr);
+            // the next step's rows are gathered by this step's update kernel
+            GatherArgs nxt;
+            const bool more = step + 1 < total;
+            if (more) {
+                const int64_t s2 = s + 1 < spe ? s + 1 : 0;
+                const int32_t ep2 = s + 1 < spe ? ep : ep + 1;
+                const int64_t off2 = s2 * batch;
+                nxt = gather_args(*c, X, Y, n, perm ? perm + (int64_t)ep2 * n : nullptr, off2,
+                                  n - off2 < batch ? n - off2 : batch);
+            }
+            e = deep_step(*c, X, n, Y, ix, off, nb, a, nullptr, step > 0, more ? &nxt : nullptr);
             if (e != hipSuccess) break;
             ++step;
         }
