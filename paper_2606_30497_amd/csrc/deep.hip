@@ -370,7 +370,7 @@ __global__ __launch_bounds__(256) void k_deep_ypred(const float *__restrict__ H,
 }
 
 // Output layer of a training step over row chunk z = blockIdx.x (rows [z kc,
-// min(nb, z kc + kc))); wave w takes rows w, w + 4, ... of the chunk and lane l
+// min(nb, z kc + kc))); wave w of OUT_W takes rows w, w + OUT_W, ... of the chunk and lane l
 // units l, l + 64, ... (HU of them). Per row: Ypred = H_L w_o (eq. 13),
 // r = Ypred - Y, r^2, dZ_o = (2/n_b) r (eq. 15) and G_L = dZ_o w_o^T (.)
 // [H_L > 0] (eq. 17); each lane also sums H_L[r][j] dZ_o[r] over its rows in
@@ -378,14 +378,15 @@ __global__ __launch_bounds__(256) void k_deep_ypred(const float *__restrict__ H,
 // the chunk's dw_o partial. A wave loads OUT_R rows before it reduces any of
 // them, so that their loads are in flight together.
 constexpr int OUT_R = 4;
+constexpr int OUT_W = 8;   // waves per workgroup of the output kernel
 template <int HU>
-__global__ __launch_bounds__(256) void k_deep_out(const float *__restrict__ H, int h,
+__global__ __launch_bounds__(64 * OUT_W) void k_deep_out(const float *__restrict__ H, int h,
                                                   const float *__restrict__ wo,
                                                   const float *__restrict__ Yb, int64_t nb,
                                                   int64_t kc, float scale, float *__restrict__ sq,
                                                   float *__restrict__ Gout,
                                                   float *__restrict__ dwo_part) {
-    __shared__ float wsum[4][64 * HU];
+    __shared__ float wsum[OUT_W][64 * HU];
     const int lane = threadIdx.x & 63, wave = threadIdx.x >> 6;
     const int64_t rb = (int64_t)blockIdx.x * kc;
     const int64_t re = rb + kc < nb ? rb + kc : nb;
@@ -395,12 +396,12 @@ __global__ __launch_bounds__(256) void k_deep_out(const float *__restrict__ H, i
         wov[i] = wo[lane + 64 * i];
         acc[i] = 0.0f;
     }
-    for (int64_t r0 = rb + wave; r0 < re; r0 += 4 * OUT_R) {
+    for (int64_t r0 = rb + wave; r0 < re; r0 += OUT_W * OUT_R) {
         // rows past the chunk load its last row and are dropped below
         float hv[OUT_R][HU], yv[OUT_R];
 #pragma unroll
         for (int j = 0; j < OUT_R; ++j) {
-            const int64_t r = r0 + 4 * j < re ? r0 + 4 * j : re - 1;
+            const int64_t r = r0 + OUT_W * j < re ? r0 + OUT_W * j : re - 1;
             const float *hr = H + r * h;
 #pragma unroll
             for (int i = 0; i < HU; ++i) hv[j][i] = hr[lane + 64 * i];
@@ -408,7 +409,7 @@ __global__ __launch_bounds__(256) void k_deep_out(const float *__restrict__ H, i
         }
 #pragma unroll
         for (int j = 0; j < OUT_R; ++j) {
-            const int64_t r = r0 + 4 * j;
+            const int64_t r = r0 + OUT_W * j;
             float s = 0.0f;
 #pragma unroll
             for (int i = 0; i < HU; ++i) s = fmaf(hv[j][i], wov[i], s);
@@ -428,8 +429,12 @@ __global__ __launch_bounds__(256) void k_deep_out(const float *__restrict__ H, i
 #pragma unroll
     for (int i = 0; i < HU; ++i) wsum[wave][lane + 64 * i] = acc[i];
     __syncthreads();
-    for (int j = threadIdx.x; j < h; j += 256)
-        dwo_part[(int64_t)blockIdx.x * h + j] = ((wsum[0][j] + wsum[1][j]) + wsum[2][j]) + wsum[3][j];
+    for (int j = threadIdx.x; j < h; j += 64 * OUT_W) {
+        float v = wsum[0][j];
+#pragma unroll
+        for (int w = 1; w < OUT_W; ++w) v += wsum[w][j];
+        dwo_part[(int64_t)blockIdx.x * h + j] = v;
+    }
 }
 
 // Row-chunk split of each parameter segment's gradient (W_1 .. W_L, then w_o).
@@ -709,7 +714,7 @@ static hipError_t launch_out(const DeepCtx &c, const float *HL, const float *wo,
     switch (c.hidden / 64) {
 #define DEEP_OUT_CASE(U)                                                                          \
     case U:                                                                                       \
-        hipLaunchKernelGGL((k_deep_out<U>), dim3(chunks), dim3(256), 0, c.stream, HL, c.hidden, wo, \
+        hipLaunchKernelGGL((k_deep_out<U>), dim3(chunks), dim3(64 * OUT_W), 0, c.stream, HL, c.hidden, wo, \
                            c.Yb, nb, kc, scale, c.sq, c.G[0], dwo_part);                           \
         return hipGetLastError();
         DEEP_OUT_CASE(1) DEEP_OUT_CASE(2) DEEP_OUT_CASE(3) DEEP_OUT_CASE(4)
