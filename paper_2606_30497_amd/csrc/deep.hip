@@ -374,7 +374,7 @@ __global__ __launch_bounds__(256) void k_deep_ypred(const float *__restrict__ H,
 // units l, l + 64, ... (HU of them). Per row: Ypred = H_L w_o (eq. 13),
 // r = Ypred - Y, r^2, dZ_o = (2/n_b) r (eq. 15) and G_L = dZ_o w_o^T (.)
 // [H_L > 0] (eq. 17); each lane also sums H_L[r][j] dZ_o[r] over its rows in
-// row order (eq. 16), and the four waves' sums are added in wave order into
+// row order (eq. 16), and the OUT_W waves' sums are added in wave order into
 // the chunk's dw_o partial. A wave loads OUT_R rows before it reduces any of
 // them, so that their loads are in flight together.
 constexpr int OUT_R = 4;
