@@ -359,13 +359,16 @@ FUSED_SHAPES = [(8, 32, 128, 32), (8, 32, 64, 32), (8, 32, 32, 32), (4, 32, 16, 
                 (4, 16, 16, 64), (2, 16, 16, 128), (4, 4, 16, 64), (8, 4, 32, 32),
                 (8, 8, 32, 32)]
 # Index = position in the library's shape table. A one-XCD shape with four
-# workgroups of 64 owned units each, (1, 4, 16, 256), is disabled: its
-# gradient sums came out wrong from the second SGD step on, and one run of it
-# faulted the GPU; the cause is not found yet, so it is not instantiated.
+# workgroups of 64 owned units each, (1, 4, 16, 256), gave wrong gradient sums
+# from the second SGD step on, and one run of it faulted the GPU, under the
+# kernel's first ownership scheme; the cause was not found. The owner waves of
+# the current kernel cap a workgroup at 16 owned units (a compile-time
+# assertion), so the shape is not instantiated.
 
 
-@pytest.mark.skip(reason="shape (1, 4, 16, 256) disabled: wrong sums from step 2 and one GPU "
-                         "fault, cause not yet found; not instantiated in the library")
+@pytest.mark.skip(reason="shape (1, 4, 16, 256) excluded: failed under the first ownership "
+                         "scheme (cause not found); the current one owns at most 16 units "
+                         "per workgroup, so it is not instantiated")
 def test_disabled_shape_four_workgroups_one_xcd():
     pass
 
