@@ -378,7 +378,8 @@ __global__ __launch_bounds__(256) void k_deep_ypred(const float *__restrict__ H,
 // the chunk's dw_o partial. A wave loads OUT_R rows before it reduces any of
 // them, so that their loads are in flight together.
 constexpr int OUT_R = 4;
-constexpr int OUT_W = 8;   // waves per workgroup of the output kernel
+constexpr int OUT_W = 8;                   // waves per workgroup of the output kernel
+constexpr int OUT_ROWS = OUT_W * OUT_R;    // rows of one output-kernel pass (chunk granule)
 template <int HU>
 __global__ __launch_bounds__(64 * OUT_W) void k_deep_out(const float *__restrict__ H, int h,
                                                   const float *__restrict__ wo,
@@ -569,7 +570,7 @@ static bool deep_shape_ok(int32_t d_in, int32_t hidden, int32_t layers) {
 // Row chunks of segment s's gradient before rounding the chunk length: a weight
 // segment W_l gets enough chunks for its GEMM to reach about 512 workgroups
 // (output tiles x chunks), at most SPLIT_MAX, with at least 64 rows a chunk; w_o
-// gets one chunk per 32 rows of the output kernel, at most OUT_CHUNKS_MAX. This
+// gets one chunk per OUT_ROWS rows of the output kernel, at most OUT_CHUNKS_MAX. This
 // count never falls as nb grows, and the chunks a plan uses never exceed it, so
 // the count at max_batch sizes the partial buffer for every batch.
 static int64_t seg_chunks(int h, int L, int64_t nb, int s) {
@@ -582,7 +583,7 @@ static int64_t seg_chunks(int h, int L, int64_t nb, int s) {
         if (splits > by_rows) splits = by_rows;
         splits = splits > SPLIT_MAX ? SPLIT_MAX : splits;
     } else {
-        splits = (nb + 31) / 32;
+        splits = (nb + OUT_ROWS - 1) / OUT_ROWS;
         splits = splits > OUT_CHUNKS_MAX ? OUT_CHUNKS_MAX : splits;
     }
     return splits < 1 ? 1 : splits;
@@ -600,14 +601,16 @@ static int64_t part_layout(int h, int L, int64_t mb, int64_t *off) {
     return o;
 }
 
-// The plan of a batch of nb rows: chunk length rounded up to the GEMM's K chunk,
-// and the chunk count that length gives (never more than seg_chunks).
+// The plan of a batch of nb rows: chunk length rounded up to the GEMM's K chunk
+// (to the output kernel's pass for w_o), and the chunk count that length gives
+// (never more than seg_chunks).
 static void split_plan(int h, int L, int64_t nb, const int64_t *part_off, SplitPlan *sp) {
     sp->nseg = L + 1;
     for (int s = 0; s <= L; ++s) {
         const int64_t splits = seg_chunks(h, L, nb, s);
         int64_t c = (nb + splits - 1) / splits;
-        c = (c + GK - 1) / GK * GK;
+        const int64_t q = s < L ? GK : OUT_ROWS;
+        c = (c + q - 1) / q * q;
         sp->kc[s] = c;
         sp->splits[s] = (int)((nb + c - 1) / c);
         sp->seg_end[s] = s < L ? layer_offset(h, s + 2) : deep_np(h, L);
