@@ -29,7 +29,7 @@
 // Every output element is one lane's sum in a fixed order, so results are
 // bitwise reproducible.
 //
-// GEMM tile: 64 x 64 (or 32 x 64) outputs per workgroup of four waves (each a
+// GEMM tile: 64 x 64 (or 32 x 64, 32 x 32) outputs per workgroup of four waves (each a
 // quarter, as 16 x 16 v_mfma_f32_16x16x4f32 tiles), K in chunks of 32 staged in
 // LDS (operands read along m or n stored k-major with a row stride of TM + 16
 // floats, operands read along k as loaded with a stride of 34, so that MFMA
@@ -153,7 +153,7 @@ __device__ __forceinline__ void gemm_stash(const Stage<TM, TN> &st, float *As, f
 //   NN: a(m, k) = A[m lda + k],  b(k, n) = B[k ldb + n]
 //   TN: a(m, k) = A[k lda + m],  b(k, n) = B[k ldb + n]
 //   NT: a(m, k) = A[m lda + k],  b(k, n) = B[n ldb + k]
-// Output tile TM x TN (launched as 32 x 64 or 64 x 64); each of the four waves
+// Output tile TM x TN (launched as 32 x 32, 32 x 64 or 64 x 64); each of the four waves
 // computes a TM/2 x TN/2 quarter as (TM/32) x (TN/32) MFMA tiles of 16 x 16.
 // Grid: (ceil(M/TM), ceil(N/TN), splits); split z covers k in [z kc, min(K,
 // z kc + kc)) and writes C + z * c_split. N and the contiguous dimension of
@@ -628,7 +628,8 @@ static size_t deep_ws_floats(int h, int L, int64_t mb) {
 
 // Tile choice: 64 x 64, or 32 x 64 where 64-row tiles would leave fewer than
 // two workgroups per CU (the 256-wide layers) or M itself is 32 (the weight
-// gradient of W_1). Larger tiles (128 x 64, 128 x 128) halve the operand
+// gradient of W_1); a single product (not a pair) narrows that to 32 x 32 where
+// it would still leave fewer than four. Larger tiles (128 x 64, 128 x 128) halve the operand
 // traffic per MFMA but leave one or two workgroups per CU on the 1024-wide
 // products, which measured 6-8 % slower than four.
 static GemmArgs gemm_args(const float *A, int lda, const float *B, int ldb, float *C, int ldc,
@@ -664,7 +665,14 @@ static hipError_t gemm(hipStream_t st, const float *A, int lda, const float *B, 
     bool small;
     const GemmArgs g = gemm_args(A, lda, B, ldb, C, ldc, c_split, M, N, K, splits, kc, G, ldg, &small);
     const dim3 grid((unsigned)g.gx, (unsigned)g.gy, (unsigned)g.gz);
-    if (small)
+    if (small && (int64_t)g.gx * g.gy * g.gz < 4 * GEMM_CUS) {
+        // 32 x 32 tiles where 32 x 64 ones would leave fewer than four
+        // workgroups per CU
+        GemmArgs gn = g;
+        gn.gy = (N + 31) / 32;
+        hipLaunchKernelGGL((k_gemm<OP, EP, 32, 32>), dim3((unsigned)gn.gx, (unsigned)gn.gy, (unsigned)gn.gz),
+                           dim3(256), 0, st, gn);
+    } else if (small)
         hipLaunchKernelGGL((k_gemm<OP, EP, 32, GT>), grid, dim3(256), 0, st, g);
     else
         hipLaunchKernelGGL((k_gemm<OP, EP, GT, GT>), grid, dim3(256), 0, st, g);
