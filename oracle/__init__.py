@@ -15,6 +15,12 @@ of an all-active (linear) net, a hand-worked two-sample step, the strict
 ReLU'(0) = 0 convention, torch float64 autograd at the real shapes, and
 invariants of the batch-size scaling.
 
+``oracle_mt.c`` (liboracle_mt.so, OpenMP) is the same SGD with each batch cut
+into 64 fixed row chunks whose partials are summed in chunk order, so its
+result does not depend on the thread count; the ``mt_*`` functions marshal into
+it. Pinned to the single-thread oracle (tests/test_oracle_mt.py): forward
+bitwise equal, gradients and 10-step training within 1e-13.
+
 ``oracle_deep.c`` (its own library, liboracle_deep.so, sharing no code with
 oracle.c) extends the same equations to L hidden layers of width h; the
 ``deep_*`` functions below marshal into it. Its pins
@@ -35,29 +41,34 @@ _SRC = os.path.join(_HERE, "oracle.c")
 _LIB = os.path.join(_HERE, "liboracle.so")
 _DEEP_SRC = os.path.join(_HERE, "oracle_deep.c")
 _DEEP_LIB = os.path.join(_HERE, "liboracle_deep.so")
+_MT_SRC = os.path.join(_HERE, "oracle_mt.c")
+_MT_LIB = os.path.join(_HERE, "liboracle_mt.so")
 _lib = None
 _deep_lib = None
+_mt_lib = None
 
 _f32p = np.ctypeslib.ndpointer(np.float32, flags="C_CONTIGUOUS")
 _f64p = np.ctypeslib.ndpointer(np.float64, flags="C_CONTIGUOUS")
 _i32p = np.ctypeslib.ndpointer(np.int32, flags="C_CONTIGUOUS")
 
 
-def _gcc(src, lib):
+def _gcc(src, lib, extra=()):
     tmp = lib + ".tmp%d" % os.getpid()
     subprocess.check_call(["gcc", "-O2", "-std=c11", "-fPIC", "-shared",
-                           "-ffp-contract=off", "-fno-fast-math", "-Wall",
+                           "-ffp-contract=off", "-fno-fast-math", "-Wall", *extra,
                            "-o", tmp, src, "-lm"])
     os.replace(tmp, lib)
 
 
 def build(force: bool = True) -> str:
-    """Compile liboracle.so and liboracle_deep.so with gcc (plain -O2, no FMA
-    contraction, no fast-math)."""
+    """Compile liboracle.so, liboracle_deep.so and liboracle_mt.so (OpenMP) with
+    gcc (plain -O2, no FMA contraction, no fast-math)."""
     if force or not os.path.exists(_LIB):
         _gcc(_SRC, _LIB)
     if force or not os.path.exists(_DEEP_LIB):
         _gcc(_DEEP_SRC, _DEEP_LIB)
+    if force or not os.path.exists(_MT_LIB):
+        _gcc(_MT_SRC, _MT_LIB, ("-fopenmp",))
     return _LIB
 
 
@@ -184,6 +195,110 @@ def train(X, Y, W1, W2, batch, lr, epochs, perm=None, max_steps=-1):
                               max_steps, _ptr(step_loss), _ptr(epoch_loss), ctypes.byref(steps))
     if rc != 0:
         raise ValueError("oracle_train failed: %d" % rc)
+    return dict(W1=W1, W2=W2, step_loss=step_loss[:steps.value],
+                epoch_loss=epoch_loss[:epochs], steps=steps.value)
+
+
+# --- the same SGD on several host cores (oracle_mt.c) ------------------------------
+
+def _load_mt():
+    global _mt_lib
+    if _mt_lib is None:
+        if not os.path.exists(_MT_LIB):
+            _gcc(_MT_SRC, _MT_LIB, ("-fopenmp",))
+        lib = ctypes.CDLL(_MT_LIB)
+        lib.oracle_mt_threads.restype = ctypes.c_int
+        lib.oracle_mt_threads.argtypes = []
+        lib.oracle_mt_set_threads.restype = ctypes.c_int
+        lib.oracle_mt_set_threads.argtypes = [ctypes.c_int]
+        lib.oracle_mt_forward.restype = ctypes.c_int
+        lib.oracle_mt_forward.argtypes = [_f32p, ctypes.c_int64, ctypes.c_void_p, ctypes.c_int64,
+                                          ctypes.c_int32, ctypes.c_int32, _f64p, _f64p, _f64p]
+        lib.oracle_mt_grad.restype = ctypes.c_int
+        lib.oracle_mt_grad.argtypes = [_f32p, _f32p, ctypes.c_int64, ctypes.c_void_p,
+                                       ctypes.c_int64, ctypes.c_int32, ctypes.c_int32, _f64p,
+                                       _f64p, _f64p, _f64p, ctypes.POINTER(ctypes.c_double)]
+        lib.oracle_mt_train.restype = ctypes.c_int
+        lib.oracle_mt_train.argtypes = [_f32p, _f32p, ctypes.c_int64, ctypes.c_int32,
+                                        ctypes.c_int32, _f64p, _f64p, ctypes.c_int64,
+                                        ctypes.c_double, ctypes.c_int32, ctypes.c_void_p,
+                                        ctypes.c_int64, ctypes.c_void_p, ctypes.c_void_p,
+                                        ctypes.POINTER(ctypes.c_int64)]
+        _mt_lib = lib
+    return _mt_lib
+
+
+def mt_threads():
+    """Threads the multi-core oracle runs on (OMP_NUM_THREADS, else every core
+    the process may use)."""
+    return int(_load_mt().oracle_mt_threads())
+
+
+def mt_set_threads(n):
+    """Run the following multi-core oracle calls on n threads; returns the
+    previous count."""
+    return int(_load_mt().oracle_mt_set_threads(int(n)))
+
+
+def mt_forward(X, W1, W2, idx=None, nb=None):
+    """forward() on every host core: the same values, row by row."""
+    X = np.ascontiguousarray(X, dtype=np.float32)
+    W1 = np.ascontiguousarray(W1, dtype=np.float64)
+    W2 = np.ascontiguousarray(np.reshape(W2, -1), dtype=np.float64)
+    idx = _idx(idx)
+    d, h = W1.shape
+    if nb is None:
+        nb = X.shape[0] if idx is None else idx.shape[0]
+    out = np.empty(nb, dtype=np.float64)
+    rc = _load_mt().oracle_mt_forward(X, X.shape[0], _ptr(idx), nb, d, h, W1, W2, out)
+    if rc != 0:
+        raise ValueError("oracle_mt_forward failed: %d" % rc)
+    return out
+
+
+def mt_grad(X, Y, W1, W2, idx=None, nb=None):
+    """grad() with each batch cut into 64 row chunks summed in chunk order:
+    returns (dW1, dW2, loss)."""
+    X = np.ascontiguousarray(X, dtype=np.float32)
+    Y = np.ascontiguousarray(np.reshape(Y, -1), dtype=np.float32)
+    W1 = np.ascontiguousarray(W1, dtype=np.float64)
+    W2 = np.ascontiguousarray(np.reshape(W2, -1), dtype=np.float64)
+    idx = _idx(idx)
+    d, h = W1.shape
+    if nb is None:
+        nb = X.shape[0] if idx is None else idx.shape[0]
+    dW1 = np.empty((d, h), dtype=np.float64)
+    dW2 = np.empty(h, dtype=np.float64)
+    loss = ctypes.c_double(0.0)
+    rc = _load_mt().oracle_mt_grad(X, Y, X.shape[0], _ptr(idx), nb, d, h, W1, W2, dW1, dW2,
+                                   ctypes.byref(loss))
+    if rc != 0:
+        raise ValueError("oracle_mt_grad failed: %d" % rc)
+    return dW1, dW2, loss.value
+
+
+def mt_train(X, Y, W1, W2, batch, lr, epochs, perm=None, max_steps=-1):
+    """train() with chunked batch gradients on every host core; same outputs."""
+    X = np.ascontiguousarray(X, dtype=np.float32)
+    Y = np.ascontiguousarray(np.reshape(Y, -1), dtype=np.float32)
+    W1 = np.array(W1, dtype=np.float64, order="C", copy=True)
+    W2 = np.array(np.reshape(W2, -1), dtype=np.float64, copy=True)
+    n = X.shape[0]
+    d, h = W1.shape
+    if perm is not None:
+        perm = np.ascontiguousarray(perm, dtype=np.int32)
+        if perm.shape != (epochs, n):
+            raise ValueError("perm must be [epochs, n]")
+    spe = -(-n // batch)
+    total = spe * epochs if max_steps < 0 else min(max_steps, spe * epochs)
+    step_loss = np.zeros(max(total, 1), dtype=np.float64)
+    epoch_loss = np.zeros(max(epochs, 1), dtype=np.float64)
+    steps = ctypes.c_int64(0)
+    rc = _load_mt().oracle_mt_train(X, Y, n, d, h, W1, W2, batch, float(lr), epochs,
+                                    _ptr(perm), max_steps, _ptr(step_loss), _ptr(epoch_loss),
+                                    ctypes.byref(steps))
+    if rc != 0:
+        raise ValueError("oracle_mt_train failed: %d" % rc)
     return dict(W1=W1, W2=W2, step_loss=step_loss[:steps.value],
                 epoch_loss=epoch_loss[:epochs], steps=steps.value)
 
