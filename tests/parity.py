@@ -1,6 +1,10 @@
 """Comparison helpers for GPU-vs-oracle parity (test infrastructure).
 
-Relative error is normwise: ||a - ref||_F / ||ref||_F.
+Relative error is normwise: ||a - ref||_F / ||ref||_F (rel). Next to it every
+check also computes the largest elementwise error against the largest
+reference entry, max|a - ref| / max|ref| (relmax), so that a few entries far
+off cannot hide under a small normwise error; check() reports both and holds
+both to the bar.
 
 ReLU kink: where a pre-activation Z1[i, j] is so close to zero that fp32
 cannot resolve its sign, both mask values are correct results of eq. (17).
@@ -25,6 +29,22 @@ def rel(a, ref):
     ref = np.asarray(ref, np.float64)
     den = np.linalg.norm(ref)
     return float(np.linalg.norm(a - ref) / (den if den > 0 else 1.0))
+
+
+def relmax(a, ref):
+    a = np.asarray(a, np.float64)
+    ref = np.asarray(ref, np.float64)
+    den = float(np.max(np.abs(ref))) if ref.size else 0.0
+    return float(np.max(np.abs(a - ref)) / (den if den > 0 else 1.0)) if ref.size else 0.0
+
+
+def check(name, a, ref, bar):
+    """Assert rel(a, ref) <= bar and relmax(a, ref) <= bar; print both."""
+    e, m = rel(a, ref), relmax(a, ref)
+    print("%-24s rel %.3e  relmax %.3e  (bar %.0e)" % (name, e, m, bar), flush=True)
+    assert e <= bar, (name, "normwise", e, bar)
+    assert m <= bar, (name, "max elementwise", m, bar)
+    return e, m
 
 
 def align_kinks(dW1_gpu, dW1_ref, X, Y, W1, W2, idx, z, zabs, ypred):

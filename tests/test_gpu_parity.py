@@ -4,13 +4,16 @@ Tolerances (normwise relative error unless stated):
   - per-step gradients dW1, dW2: <= 1e-4, after ReLU-kink alignment of dW1;
   - forward outputs: <= 1e-5; batch loss: 1e-5 relative plus the fp32 forward
     rounding term of tests/parity.py:loss_tolerance (matters where Ypred ~ Y);
-  - weights and per-step losses after 10 SGD steps: <= 1e-3. The weight change
-    W10 - W0 is also held to 1e-3, which is the meaningful check since
-    lr * dW is small against W. The 32-1024-1 workload at lr 0.005 is the
-    exception: its first steps are a divergent transient (the loss grows by
-    about five orders of magnitude), and its 10-step map amplifies a relative
-    perturbation of 1e-6 in W0 to about 1.4e-3 in W1 (measured with the oracle
-    alone), so no fp32 implementation can meet 1e-3 there; its W1 bar is 1e-2.
+  - weights and per-step losses after 10 SGD steps: <= 1e-3, on every
+    workload, and so is the weight change W10 - W0 (the meaningful check, since
+    lr * dW is small against W);
+  - the full-dataset MSE at the weights after those 10 steps, the GPU's own
+    forward pass over every row (mlp_forward) against the oracle's forward at
+    the oracle's weights: <= 1e-3 relative;
+  - gradients at trained weights (after 10 steps of the largest workload): the
+    per-step bar, 1e-4.
+Every weight and gradient check holds both the normwise and the largest
+elementwise error (tests/parity.py:check) to its bar.
 """
 import numpy as np
 import pytest
@@ -18,7 +21,7 @@ import torch
 
 import datagen
 import oracle
-from tests.parity import align_kinks, loss_tolerance, rel
+from tests.parity import align_kinks, check, loss_tolerance, rel
 
 pytestmark = pytest.mark.gpu
 
@@ -120,9 +123,9 @@ def _check_grad(mlp, h, B, n=5000, seed=0, idx_none=False, strategy=None):
     r1, r2, rL, z, zabs = oracle.grad(d.X, d.Y, W1, W2, idx=idx, nb=B, want_z=True)
     yp = oracle.forward(d.X, W1, W2, idx=idx, nb=B)
     r1a, n_amb, flips = align_kinks(g1, r1, d.X, d.Y, W1, W2, idx, z, zabs, yp)
-    e1, e2 = rel(g1, r1a), rel(g2, r2)
-    assert e1 <= 1e-4, (e1, n_amb, flips)
-    assert e2 <= 1e-4, e2
+    print("kink entries %d, flips accepted %d" % (n_amb, flips))
+    e1, _ = check("dW1", g1, r1a, 1e-4)
+    e2, _ = check("dW2", g2, r2, 1e-4)
     assert abs(gl - rL) <= loss_tolerance(rL, z, zabs, W2)
     return e1, e2
 
@@ -214,22 +217,63 @@ def _train_gpu(mlp, d, batch, lr, epochs, max_steps=-1, perm=None, strategy=None
     return w1.cpu().numpy(), w2.cpu().numpy(), sl.cpu().numpy(), el.cpu().numpy()
 
 
-W1_BAR = {3: 1e-2}
-
-
 @pytest.mark.parametrize("k", range(5))
 def test_train_ten_steps_full_workload(mlp, k):
     w, d = _workload_data(k)
     print("workload", w.name, flush=True)
-    g1, g2, gsl, _ = _train_gpu(mlp, d, w.batch, w.lr, w.epochs, max_steps=10, perm=d.perm)
+    ctx, w1, w2 = _ctx(mlp, d.W1, d.W2, w.batch)
+    sl = torch.zeros(10, dtype=torch.float32, device="cuda")
+    X, Y = _to(d.X), _to(d.Y)
+    perm = None if d.perm is None else _to(d.perm)
+    mlp.mlp_train_epochs(ctx, X, Y, w.batch, w.lr, w.epochs, perm=perm, max_steps=10,
+                         step_loss=sl)
+    torch.cuda.synchronize()
+    mlp.mlp_check_errors(ctx)
+    g1, g2, gsl = w1.cpu().numpy(), w2.cpu().numpy(), sl.cpu().numpy()
     ref = oracle.train(d.X, d.Y, d.W1, d.W2, w.batch, w.lr, w.epochs, perm=d.perm, max_steps=10)
-    bar1 = W1_BAR.get(k, 1e-3)
-    assert rel(g1, ref["W1"]) <= bar1
-    assert rel(g2, ref["W2"]) <= 1e-3
-    W10 = d.W1.astype(np.float64)
-    assert rel(g1 - W10, ref["W1"] - W10) <= max(bar1, 1e-3)
-    assert rel(g2 - d.W2, ref["W2"] - d.W2.astype(np.float64)) <= 1e-3
+    W10, W20 = d.W1.astype(np.float64), d.W2.astype(np.float64)
+    check("W1", g1, ref["W1"], 1e-3)
+    check("W2", g2, ref["W2"], 1e-3)
+    check("W1 - W1_0", g1 - W10, ref["W1"] - W10, 1e-3)
+    check("W2 - W2_0", g2 - W20, ref["W2"] - W20, 1e-3)
     assert np.all(np.abs(gsl - ref["step_loss"]) <= 1e-3 * np.abs(ref["step_loss"]))
+    # full-dataset MSE at the trained weights: the GPU's forward pass over every
+    # row (eqs. 11-14) against the oracle's forward at the oracle's weights
+    yp = mlp.mlp_forward(ctx, X).cpu().numpy().astype(np.float64)
+    mse_gpu = float(np.mean((yp - d.Y) ** 2))
+    mse_ref = float(np.mean((oracle.mt_forward(d.X, ref["W1"], ref["W2"]) - d.Y) ** 2))
+    print("full-dataset MSE at W10: gpu %.6e oracle %.6e rel %.3e" %
+          (mse_gpu, mse_ref, abs(mse_gpu - mse_ref) / mse_ref))
+    assert abs(mse_gpu - mse_ref) <= 1e-3 * mse_ref
+
+
+def test_gradients_at_trained_weights(mlp):
+    """Per-step gradients of the largest workload at the weights its first 10 SGD
+    steps on the GPU reached (not only at the initial weights): a full batch of
+    4096 rows and the 1664-row tail size, each against the oracle at the same
+    fp32 weights, kink-aligned, <= 1e-4."""
+    w, d = _workload_data(4)
+    ctx, w1, w2 = _ctx(mlp, d.W1, d.W2, w.batch)
+    X, Y = _to(d.X), _to(d.Y)
+    mlp.mlp_train_epochs(ctx, X, Y, w.batch, w.lr, w.epochs, perm=_to(d.perm), max_steps=10)
+    torch.cuda.synchronize()
+    mlp.mlp_check_errors(ctx)
+    W1t = w1.cpu().numpy().astype(np.float64)
+    W2t = w2.cpu().numpy().astype(np.float64)
+    rng = np.random.default_rng(5)
+    for B in (4096, 1664):
+        idx = rng.integers(0, w.n, size=B).astype(np.int32)
+        dW1, dW2, loss = mlp.mlp_backward(ctx, X, Y, _to(idx), B=B)
+        torch.cuda.synchronize()
+        mlp.mlp_check_errors(ctx)
+        g1, g2, gl = dW1.cpu().numpy(), dW2.cpu().numpy(), float(loss.cpu()[0])
+        r1, r2, rL, z, zabs = oracle.grad(d.X, d.Y, W1t, W2t, idx=idx, want_z=True)
+        yp = oracle.forward(d.X, W1t, W2t, idx=idx)
+        r1a, n_amb, flips = align_kinks(g1, r1, d.X, d.Y, W1t, W2t, idx, z, zabs, yp)
+        print("B %d: kink entries %d, flips accepted %d" % (B, n_amb, flips))
+        check("dW1 (trained, B=%d)" % B, g1, r1a, 1e-4)
+        check("dW2 (trained, B=%d)" % B, g2, r2, 1e-4)
+        assert abs(gl - rL) <= loss_tolerance(rL, z, zabs, W2t)
 
 
 @pytest.mark.parametrize("w", datagen.SWEEP, ids=lambda w: w.name)
@@ -240,8 +284,8 @@ def test_sweep_workload_steps(mlp, w):
     g1, g2, gsl, gel = _train_gpu(mlp, d, w.batch, w.lr, w.epochs, max_steps=20, perm=d.perm)
     ref = oracle.train(d.X, d.Y, d.W1, d.W2, w.batch, w.lr, w.epochs, perm=d.perm, max_steps=20)
     W10 = d.W1.astype(np.float64)
-    assert rel(g1 - W10, ref["W1"] - W10) <= 1e-3
-    assert rel(g2 - d.W2, ref["W2"] - d.W2.astype(np.float64)) <= 1e-3
+    check("W1 - W1_0", g1 - W10, ref["W1"] - W10, 1e-3)
+    check("W2 - W2_0", g2 - d.W2, ref["W2"] - d.W2.astype(np.float64), 1e-3)
     assert np.all(np.abs(gsl - ref["step_loss"]) <= 1e-3 * np.abs(ref["step_loss"]))
     assert np.all(np.abs(gel[:2] - ref["epoch_loss"][:2]) <= 1e-3 * ref["epoch_loss"][:2])
 
@@ -252,8 +296,8 @@ def test_train_epochs_with_tail_and_shuffle(mlp):
     g1, g2, gsl, gel = _train_gpu(mlp, d, B, lr, E, perm=d.perm)
     ref = oracle.train(d.X, d.Y, d.W1, d.W2, B, lr, E, perm=d.perm)
     assert len(gsl) == ref["steps"] == 48
-    assert rel(g1 - d.W1, ref["W1"] - d.W1.astype(np.float64)) <= 1e-3
-    assert rel(g2 - d.W2, ref["W2"] - d.W2.astype(np.float64)) <= 1e-3
+    check("W1 - W1_0", g1 - d.W1, ref["W1"] - d.W1.astype(np.float64), 1e-3)
+    check("W2 - W2_0", g2 - d.W2, ref["W2"] - d.W2.astype(np.float64), 1e-3)
     assert np.all(np.abs(gsl - ref["step_loss"]) <= 1e-3 * ref["step_loss"])
     assert np.all(np.abs(gel - ref["epoch_loss"]) <= 1e-3 * ref["epoch_loss"])
 
@@ -263,7 +307,10 @@ def test_full_first_workload_run(mlp):
     g1, g2, gsl, gel = _train_gpu(mlp, d, w.batch, w.lr, w.epochs, perm=d.perm)
     ref = oracle.train(d.X, d.Y, d.W1, d.W2, w.batch, w.lr, w.epochs, perm=d.perm)
     assert ref["steps"] == 80
-    assert rel(g1 - d.W1, ref["W1"] - d.W1.astype(np.float64)) <= 1e-3
+    check("W1 - W1_0", g1 - d.W1, ref["W1"] - d.W1.astype(np.float64), 1e-3)
+    check("W2 - W2_0", g2 - d.W2, ref["W2"] - d.W2.astype(np.float64), 1e-3)
+    check("W2", g2, ref["W2"], 1e-3)
+    assert np.all(np.abs(gsl - ref["step_loss"]) <= 1e-3 * ref["step_loss"])
     assert np.all(np.abs(gel - ref["epoch_loss"]) <= 1e-3 * ref["epoch_loss"])
 
 
@@ -395,8 +442,8 @@ def test_train_every_fused_shape(mlp, inst):
     with _env(MLP_INST=inst):
         g1, g2, gsl, gel = _train_gpu(mlp, d, B, lr, E, perm=d.perm)
     ref = oracle.train(d.X, d.Y, d.W1, d.W2, B, lr, E, perm=d.perm)
-    assert rel(g1 - d.W1, ref["W1"] - d.W1.astype(np.float64)) <= 1e-3
-    assert rel(g2 - d.W2, ref["W2"] - d.W2.astype(np.float64)) <= 1e-3
+    check("W1 - W1_0", g1 - d.W1, ref["W1"] - d.W1.astype(np.float64), 1e-3)
+    check("W2 - W2_0", g2 - d.W2, ref["W2"] - d.W2.astype(np.float64), 1e-3)
     assert np.all(np.abs(gsl - ref["step_loss"]) <= 1e-3 * ref["step_loss"])
     assert np.all(np.abs(gel - ref["epoch_loss"]) <= 1e-3 * ref["epoch_loss"])
 
@@ -421,8 +468,8 @@ def test_host_loop_strategy_matches_oracle(mlp, strategy, h, B):
     d = datagen.make_data(n, h, epochs=E, shuffle=True, seed=93 + h)
     g1, g2, gsl, gel = _train_gpu(mlp, d, B, lr, E, perm=d.perm, strategy=strategy)
     ref = oracle.train(d.X, d.Y, d.W1, d.W2, B, lr, E, perm=d.perm)
-    assert rel(g1 - d.W1, ref["W1"] - d.W1.astype(np.float64)) <= 1e-3
-    assert rel(g2 - d.W2, ref["W2"] - d.W2.astype(np.float64)) <= 1e-3
+    check("W1 - W1_0", g1 - d.W1, ref["W1"] - d.W1.astype(np.float64), 1e-3)
+    check("W2 - W2_0", g2 - d.W2, ref["W2"] - d.W2.astype(np.float64), 1e-3)
     assert np.all(np.abs(gsl - ref["step_loss"]) <= 1e-3 * ref["step_loss"])
     assert np.all(np.abs(gel - ref["epoch_loss"]) <= 1e-3 * ref["epoch_loss"])
 
