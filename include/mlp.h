@@ -181,6 +181,23 @@ mlp_status mlp_last_kernel_ms(mlp_t ctx, float *ms);
 mlp_status mlp_launch_info(mlp_t ctx, int64_t n, int64_t batch, int32_t epochs,
                            int32_t *workgroups, int64_t *launches);
 
+/* Diagnostic: where the fused trainer's SGD step spends its cycles. With
+ * MLP_TRACE=1 in the environment, a training call on the fused strategy makes
+ * compute wave 0 and the first owner wave of every workgroup sum the core
+ * cycles of each phase of the step (one SGD step, eqs. 11-19: forward operands,
+ * forward, the exchange of partial outputs across groups, backward, the
+ * reduction of the weight gradients, the update, the all-gather of the updated
+ * weights; twelve phases) over the call's steps from the eighth on, into the
+ * workspace. This call copies those sums of the context's last such call to
+ * host memory: out[(wg * 2 + wave) * 16 + i], wave 0 = compute wave 0, 1 = the
+ * owner wave; i = 0 steps summed, 1..12 the phases' cycles, 13 elapsed 100 MHz
+ * ticks, 14 elapsed core cycles (their ratio is the clock), 15 unused.
+ * out: host memory of max_words words (owned by the caller); *words receives
+ * the number the last traced call wrote (0 if none). Copies min(max_words,
+ * *words) words; blocks until the context's stream is idle. Errors:
+ * MLP_ERR_INVALID_ARG for a null context or words pointer, MLP_ERR_HIP. */
+mlp_status mlp_phase_cycles(mlp_t ctx, uint64_t *out, int64_t max_words, int64_t *words);
+
 /* Release the host-side context (the caller still owns every device buffer). */
 void mlp_destroy(mlp_t ctx);
 

@@ -87,6 +87,9 @@ extern "C" mlp_status mlp_init(mlp_t *out, int32_t d_in, int32_t hidden, int32_t
     // every word is cleared to tag 0 first: memory reused from an earlier
     // context can never present a current tag.
     const int64_t words = (int64_t)(((char *)workspace + need) - (char *)c->xch) / 8;
+    c->xch_words = words;
+    // test hook: the first step tag of this context (exercises the tag wrap)
+    if (const char *tb = getenv("MLP_TAG_BASE")) c->tag_base = (uint32_t)strtoul(tb, nullptr, 10);
     if (hipGetDevice(&c->device) != hipSuccess ||
         hipDeviceGetAttribute(&c->num_cu, hipDeviceAttributeMultiprocessorCount, c->device) !=
             hipSuccess ||
@@ -330,6 +333,16 @@ extern "C" mlp_status mlp_last_kernel_ms(mlp_t c, float *ms) {
     if (!c->ev_valid) return MLP_ERR_INVALID_ARG;
     if (hipEventSynchronize(c->ev1) != hipSuccess) return MLP_ERR_HIP;
     return hip_status(hipEventElapsedTime(ms, c->ev0, c->ev1));
+}
+
+extern "C" mlp_status mlp_phase_cycles(mlp_t c, uint64_t *out, int64_t max_words,
+                                       int64_t *words) {
+    if (!c || !words || max_words < 0) return MLP_ERR_INVALID_ARG;
+    *words = c->phase_words;
+    const int64_t n = c->phase_words < max_words ? c->phase_words : max_words;
+    if (n <= 0 || !out) return MLP_OK;
+    if (hipStreamSynchronize(c->stream) != hipSuccess) return MLP_ERR_HIP;
+    return hip_status(hipMemcpy(out, c->slots, sizeof(uint64_t) * (size_t)n, hipMemcpyDeviceToHost));
 }
 
 extern "C" mlp_status mlp_launch_info(mlp_t c, int64_t n, int64_t batch, int32_t epochs,

@@ -30,7 +30,6 @@ struct Control {
     double epoch_sse;     // tile path: running sum of squared residuals of the epoch
     int32_t pad0[60];
     int32_t reg[64];      // persistent trainer: registration / start / exit counters
-    uint64_t trace[384];  // persistent trainer: optional phase timestamps (48 steps x 8)
     uint32_t pad[128];
 };
 static_assert(sizeof(Control) <= CTL_BYTES, "control block too large");
@@ -78,8 +77,7 @@ struct TrainArgs {
     uint32_t tag_base;        // tags of this call: tag_base + step
     uint64_t timeout_ticks;   // per-wait limit in s_memrealtime ticks (100 MHz)
     int32_t force_coherent;   // 1: device-coherent stores even when placement checks out
-    uint64_t *trace;          // nullable: phase timestamps of workgroup (0, 0)
-    uint64_t *trace_all;      // nullable: phase timestamps of every workgroup, 8 steps
+    uint64_t *phase;          // nullable: per-phase cycle sums of every workgroup
     TrainPlan plan;
 };
 
@@ -96,6 +94,8 @@ struct Ctx {
     uint64_t *xch = nullptr;  // persistent trainer exchange buffers
     uint64_t *rs = nullptr;
     uint64_t *ag = nullptr;
+    int64_t xch_words = 0;    // words of the three exchange buffers (cleared to tag 0)
+    int64_t phase_words = 0;  // phase-cycle words the last traced trainer call wrote
     uint32_t tag_base = 1;
     hipStream_t stream = nullptr;
     int device = 0;

@@ -49,6 +49,7 @@
 #include "mlp.h"
 #include "lanes.h"
 #include "mlp_internal.h"
+#include "tags.h"
 
 namespace mlp {
 
@@ -268,22 +269,28 @@ struct Pos {
     }
 };
 
-// Optional phase timestamps (s_memrealtime, 100 MHz): workgroup (0, 0) for the
-// first TRACE_STEPS steps, or every workgroup for steps [16, 24).
-constexpr int TRACE_STEPS = 48;
-constexpr int TRACE_ALL_FIRST = 16, TRACE_ALL_STEPS = 8;
-#define TRACE_BY(ph, t0)                                                                   \
-    do {                                                                                   \
-        if constexpr (TR)                                                                  \
-        if (a.trace && tid == (t0) && gx == 0 && gb == 0 && s < TRACE_STEPS)               \
-            a.trace[s * 8 + (ph)] = now_ticks();                                           \
-        if constexpr (TR)                                                                  \
-        if (a.trace_all && tid == (t0) && s >= TRACE_ALL_FIRST &&                          \
-            s < TRACE_ALL_FIRST + TRACE_ALL_STEPS)                                         \
-            a.trace_all[((gx * S::PR + gb) * TRACE_ALL_STEPS + (s - TRACE_ALL_FIRST)) * 8 + \
-                        (ph)] = now_ticks();                                               \
+// Optional phase accounting (MLP_TRACE=1): compute wave 0 and the first owner
+// wave of every workgroup read the core clock (s_memtime) at the boundaries of
+// the step's phases, and sum each phase's cycles over the steps from
+// PHASE_FROM on; at the end they write, per workgroup and wave, 16 words:
+//   [0] steps summed, [1..12] cycles of the phases below, [13] elapsed
+//   s_memrealtime ticks (100 MHz) and [14] elapsed core cycles over the summed
+//   steps (their ratio is the clock), [15] 0.
+// Phases: 1 forward operands from LDS (waited for), 2 forward MFMAs, epilogue
+// and exchange-A stores, 3 exchange-A wait of row tile 0, 4 backward of tile 0
+// and exchange-A wait of tile 1, 5 backward of the last tile and the P
+// partials into LDS, 6 P barrier, 7 exchange-B stores, 8 exchange-B wait
+// (owners), 9 update and exchange-C stores (owners), 10 owners barrier,
+// 11 exchange-C gather, 12 step barrier. A phase a wave does not run counts 0.
+constexpr int PHASE_FROM = 8, PHASE_WORDS = 16;
+#define PHASE(i)                                                                   \
+    do {                                                                           \
+        if constexpr (TR) {                                                        \
+            __builtin_amdgcn_sched_barrier(0);                                     \
+            ct[i] = __builtin_amdgcn_s_memtime();                                  \
+            __builtin_amdgcn_sched_barrier(0);                                     \
+        }                                                                          \
     } while (0)
-#define TRACE(ph) TRACE_BY(ph, 0)
 
 // ---------------------------------------------------------------------------
 // The kernel
@@ -408,6 +415,9 @@ __global__ __launch_bounds__(NTHR) void k_train(const TrainArgs a) {
             // the loss is reduced one step late by wave 1 of workgroup (0, 0)
             const bool lossw = gx == 0 && gb == 0 && wave == 1;
             double epoch_sse = 0.0;
+            uint64_t ct[13] = {0, 0, 0, 0, 0, 0, 0, 0, 0, 0, 0, 0, 0};   // phase stamps
+            uint64_t cacc[PHASE_WORDS] = {0, 0, 0, 0, 0, 0, 0, 0, 0, 0, 0, 0, 0, 0, 0, 0};
+            uint64_t rt0 = 0, mt0 = 0;
             Pos cur{0, 0}, prev{0, 0};
             int nb_prev = 1;
             int done = 0;
@@ -427,7 +437,12 @@ __global__ __launch_bounds__(NTHR) void k_train(const TrainArgs a) {
                 const float *Xb = Xall + par * R * XS;
                 const float *Yb = Yall + par * R;
                 const uint32_t bB = 8u * (uint32_t)((par * PX + gx) * S::GBW);   // group block (bytes)
-                TRACE(0);
+                PHASE(0);
+                if constexpr (TR)
+                    if (s == PHASE_FROM) {
+                        rt0 = now_ticks();
+                        mt0 = ct[0];
+                    }
 
                 // deferred loss: issue the loads of the previous step's SSE partials
                 const uint32_t tag_prev = tag - 1;
@@ -450,6 +465,10 @@ __global__ __launch_bounds__(NTHR) void k_train(const TrainArgs a) {
                     w1b[u][0] = a0.x; w1b[u][1] = a0.y; w1b[u][2] = a0.z; w1b[u][3] = a0.w;
                     w1b[u][4] = a1.x; w1b[u][5] = a1.y; w1b[u][6] = a1.z; w1b[u][7] = a1.w;
                     w2v[u] = Wsl[((wu + u * WU) * 16 + li) * WS + 32];
+                }
+                if constexpr (TR) {
+                    asm volatile("s_waitcnt lgkmcnt(0)" ::: "memory");   // the weight operands
+                    PHASE(1);
                 }
                 uint32_t mbits = 0;   // bit (i*NUW + u)*4 + v
 #pragma unroll
@@ -510,7 +529,7 @@ __global__ __launch_bounds__(NTHR) void k_train(const TrainArgs a) {
                     }
                 }
                 asm volatile("" ::: "memory");
-                TRACE(1);
+                PHASE(2);
 
                 // ---- 2. exchange A, residual and backward, one row tile at a time --
                 // lane (lq, li): rows 4 lq + 2 h, 4 lq + 2 h + 1 (h = li >> 3) of the
@@ -575,6 +594,7 @@ __global__ __launch_bounds__(NTHR) void k_train(const TrainArgs a) {
                         });
                         y0 = val_of(one[0].a);
                         y1 = val_of(one[0].b);
+                        if (i == 0) PHASE(3); else PHASE(4);
                         if constexpr (PX == 8) {
                             y0 += dppf<0x141>(y0);   // row_half_mirror: lanes i, 7 - i
                             y1 += dppf<0x141>(y1);
@@ -606,7 +626,6 @@ __global__ __launch_bounds__(NTHR) void k_train(const TrainArgs a) {
                         gv[2] = hh ? g0 : o0;
                         gv[3] = hh ? g1 : o1;
                     }
-                    if (i == 0) TRACE(2);
                     // ---- 3. backward: P += X_tile^T (dZ2 (.) mask) ----------------
 #pragma unroll
                     for (int v = 0; v < 4; ++v) {
@@ -634,34 +653,62 @@ __global__ __launch_bounds__(NTHR) void k_train(const TrainArgs a) {
                             make_float4(pacc[kt][u][0], pacc[kt][u][1], pacc[kt][u][2], pacc[kt][u][3]);
                     }
 
+                if constexpr (TR) {
+                    if constexpr (PX == 1) {   // no exchange A: both of its waits count 0
+                        ct[3] = ct[2];
+                        ct[4] = ct[2];
+                    } else if constexpr (RTW == 1) {
+                        ct[4] = ct[3];
+                    }
+                }
+                PHASE(5);
                 __syncthreads();   // P partials and SSE of every wave in LDS
-                TRACE(3);
+                PHASE(6);
 
                 // ---- 4. exchange B: reduce-scatter of P inside the group ---------
                 // word (ul, k) of this workgroup goes to owner o = ul / UPW at word
                 // (o * PR + gb) * NPAIR + (ul % UPW) * 32 + k of the group block
+                {
+                    // every LDS operand of this workgroup's exchange-B words first (one
+                    // LDS round trip), then the sums and the stores
+                    constexpr int NIT = S::RSW / 512;
+                    float2 pv[NIT][WR];
+                    float sv[WR];
 #pragma unroll
-                for (int i0 = 0; i0 < S::RSW; i0 += 512) {
-                    const int i = i0 + 2 * tid;          // words i, i + 1: k even
-                    const int ul = i >> 5, k = i & 31;
-                    float v0 = 0.f, v1 = 0.f;
+                    for (int it = 0; it < NIT; ++it) {
+                        const int i = it * 512 + 2 * tid;
+                        const int ul = i >> 5, k = i & 31;
 #pragma unroll
-                    for (int w = 0; w < WR; ++w) {
-                        const float2 pv = *reinterpret_cast<const float2 *>(Pred + (w * U + ul) * PS + k);
-                        v0 += pv.x;
-                        v1 += pv.y;
+                        for (int w = 0; w < WR; ++w)
+                            pv[it][w] = *reinterpret_cast<const float2 *>(Pred + (w * U + ul) * PS + k);
                     }
-                    const int o = ul / UPW, jo = ul - o * UPW;
-                    st2(rB, bB + 8u * (uint32_t)((o * PR + gb) * NPAIR + jo * 32 + k), pack(v0, tag),
-                        pack(v1, tag), !plain);
-                }
-                if (tid == 0) {
-                    float v = 0.f;
 #pragma unroll
-                    for (int w = 0; w < WR; ++w) v += SseW[w];
-                    st1(rB, bB + 8u * (uint32_t)(PR * S::RSW + gb), pack(gx == 0 ? v : 0.f, tag), !plain);
+                    for (int w = 0; w < WR; ++w) sv[w] = SseW[w];
+#pragma unroll
+                    for (int it = 0; it < NIT; ++it) {
+                        const int i = it * 512 + 2 * tid;
+                        const int ul = i >> 5, k = i & 31;
+                        float v0 = 0.f, v1 = 0.f;
+#pragma unroll
+                        for (int w = 0; w < WR; ++w) {
+                            v0 += pv[it][w].x;
+                            v1 += pv[it][w].y;
+                        }
+                        const int o = ul / UPW, jo = ul - o * UPW;
+                        st2(rB, bB + 8u * (uint32_t)((o * PR + gb) * NPAIR + jo * 32 + k), pack(v0, tag),
+                            pack(v1, tag), !plain);
+                    }
+                    if (tid == 0) {
+                        float v = 0.f;
+#pragma unroll
+                        for (int w = 0; w < WR; ++w) v += sv[w];
+                        st1(rB, bB + 8u * (uint32_t)(PR * S::RSW + gb), pack(gx == 0 ? v : 0.f, tag), !plain);
+                    }
                 }
                 asm volatile("" ::: "memory");
+                PHASE(7);
+                ct[8] = ct[7];
+                ct[9] = ct[7];
                 if (owner) {
                     // words (k0, k0 + 1) of unit jl from sources sg * LPS + b, in source order
                     // (in chunks of at most 8 sources, to bound registers)
@@ -690,7 +737,7 @@ __global__ __launch_bounds__(NTHR) void k_train(const TrainArgs a) {
                         p0 = xadd32(p0);
                         p1 = xadd32(p1);
                     }
-                    TRACE_BY(4, OW0 * 64);
+                    PHASE(8);
                     // ---- update the owned units (eq. 19) or emit gradients ------
                     const float dw1a = ow2 * p0, dw1b = ow2 * p1;       // dW1_kj = W2_j P_kj
                     const float dw2 = rsum16(fmaf(ow1b, p1, ow1a * p0)); // dW2_j = sum_k W1_kj P_kj
@@ -712,7 +759,7 @@ __global__ __launch_bounds__(NTHR) void k_train(const TrainArgs a) {
                             if (k0 == 0) st1(rC, cb + 8u * 32u, pack(ow2, tag), !plain);
                         }
                     }
-                    TRACE_BY(5, OW0 * 64);
+                    PHASE(9);
                 }
                 asm volatile("" ::: "memory");
 
@@ -722,6 +769,7 @@ __global__ __launch_bounds__(NTHR) void k_train(const TrainArgs a) {
                 // polls would only load the L2 while exchange B is under way
                 if constexpr (S::NWO < NCW)
                     if (a.mode == 0) __syncthreads();
+                PHASE(10);
                 if (a.mode == 0) {
                     // at most CH word pairs per thread in flight, to bound registers
                     const uint32_t cbase = 8u * (uint32_t)((par * PX + gx) * U * 33);
@@ -750,13 +798,33 @@ __global__ __launch_bounds__(NTHR) void k_train(const TrainArgs a) {
                         }
                     }
                 }
-                TRACE(6);
+                PHASE(11);
                 prev = cur;
                 nb_prev = nb;
                 cur.advance(spe);
                 done = s + 1;
                 __syncthreads();   // next step's rows staged, weight slice updated
+                PHASE(12);
+                if constexpr (TR)
+                    if (s >= PHASE_FROM) {
+#pragma unroll
+                        for (int q = 1; q < 13; ++q) cacc[q] += ct[q] - ct[q - 1];
+                        cacc[0] += 1;
+                        cacc[13] = now_ticks() - rt0;
+                        cacc[14] = ct[12] - mt0;
+                    }
             }
+            if constexpr (TR)
+                if (a.phase && lane == 0) {
+                    // slot 0: compute wave 0; slot 1: the first owner wave (the same
+                    // wave when every compute wave owns units)
+#pragma unroll
+                    for (int sl = 0; sl < 2; ++sl)
+                        if (wave == (sl == 0 ? 0 : OW0))
+#pragma unroll
+                            for (int q = 0; q < PHASE_WORDS; ++q)
+                                a.phase[((gx * S::PR + gb) * 2 + sl) * PHASE_WORDS + q] = cacc[q];
+                }
 
             // ---- after the loop -----------------------------------------------------
             const bool aborted = s_flags[3] != 0;
@@ -912,11 +980,19 @@ __global__ __launch_bounds__(NTHR) void k_train(const TrainArgs a) {
 // Host side: instantiations, plan and launch
 // ---------------------------------------------------------------------------
 
+// The kernel needs every workgroup resident at once (its waits span the grid).
+// A cooperative launch guarantees that. With regular = true (a diagnostic hook
+// for profiler runs, MLP_REGULAR_LAUNCH=1) the same kernel is launched
+// normally: one workgroup per CU by its LDS request, grid <= CUs, and the
+// kernel's start barrier times out with MLP_ERR_TIMEOUT rather than wait
+// forever if some workgroup cannot start.
 template <class S>
-static hipError_t launch_shape(hipStream_t stream, TrainArgs &a) {
+static hipError_t launch_shape(hipStream_t stream, TrainArgs &a, bool regular) {
     void *args[] = {&a};
-    const void *fn = (a.trace || a.trace_all) ? reinterpret_cast<const void *>(&k_train<S, true>)
-                                              : reinterpret_cast<const void *>(&k_train<S, false>);
+    const void *fn = a.phase ? reinterpret_cast<const void *>(&k_train<S, true>)
+                             : reinterpret_cast<const void *>(&k_train<S, false>);
+    if (regular)
+        return hipLaunchKernel(fn, dim3(a.plan.grid), dim3(NTHR), args, (size_t)a.plan.lds, stream);
     return hipLaunchCooperativeKernel(fn,
                                       dim3(a.plan.grid), dim3(NTHR), args, (unsigned)a.plan.lds,
                                       stream);
@@ -1004,8 +1080,11 @@ static const TrainPlan *all_plans(int *count) {
 //                          shape this way);
 //   MLP_FORCE_COHERENT=1   device-coherent exchange stores even when every group
 //                          sits on one XCD (tested bitwise against the default);
-//   MLP_TRACE=1 / 2        per-phase s_memrealtime stamps of one workgroup / of
-//                          every workgroup into the workspace (timing analysis).
+//   MLP_TRACE=1            per-phase cycle sums of every workgroup into the
+//                          workspace (read with mlp_phase_cycles);
+//   MLP_REGULAR_LAUNCH=1   a regular launch instead of a cooperative one (the
+//                          same kernel and grid; for profiler runs, which end
+//                          with SIGSEGV after any cooperative launch).
 bool plan_train(int hidden, int64_t batch, TrainPlan *plan) {
     const char *force = getenv("MLP_PX");
     const int fpx = force ? atoi(force) : 0;
@@ -1046,19 +1125,26 @@ hipError_t launch_train(Ctx &c, TrainArgs &a) {
     a.reg = c.ctl->reg;
     a.abort = &c.ctl->abort;
     a.err = &c.ctl->err;
-    a.tag_base = c.tag_base;
     a.timeout_ticks = 200000000ull;   // 2 s
     const char *tr = getenv("MLP_TRACE");
-    a.trace = (tr && (tr[0] == '1' || tr[0] == '2')) ? c.ctl->trace : nullptr;
-    a.trace_all = (tr && tr[0] == '2') ? reinterpret_cast<uint64_t *>(c.slots) : nullptr;
+    a.phase = (tr && tr[0] == '1') ? reinterpret_cast<uint64_t *>(c.slots) : nullptr;
+    c.phase_words = a.phase ? (int64_t)a.plan.grid * 2 * PHASE_WORDS : 0;
     const char *fc = getenv("MLP_FORCE_COHERENT");
     a.force_coherent = (fc && fc[0] == '1') ? 1 : 0;
-    // tags of the next call start past every tag this call can use
-    c.tag_base += (uint32_t)(a.steps + 2);
-    if (c.tag_base < 1) c.tag_base = 1;
+    // tags of the next call start past every tag this call can use; a range
+    // that would leave 32 bits restarts at 1 over cleared exchange words
+    const TagPlan tp = plan_tags(c.tag_base, a.steps);
+    if (tp.clear) {
+        const hipError_t e = clear_words(c, c.xch, c.xch_words);
+        if (e != hipSuccess) return e;
+    }
+    a.tag_base = tp.base;
+    c.tag_base = tp.next;
+    const char *rl = getenv("MLP_REGULAR_LAUNCH");
+    const bool regular = rl && rl[0] == '1' && c.num_cu >= a.plan.grid;
     switch (a.plan.inst) {
 #define MLP_SHAPE_CASE(I, PX, PR, R, U) \
-    case I: return launch_shape<Shape##I>(c.stream, a);
+    case I: return launch_shape<Shape##I>(c.stream, a, regular);
         MLP_SHAPES(MLP_SHAPE_CASE)
 #undef MLP_SHAPE_CASE
     }

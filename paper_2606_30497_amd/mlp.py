@@ -31,7 +31,8 @@ STRATEGIES = {"fused": STRATEGY_FUSED, "tile": STRATEGY_TILE, "optimized": STRAT
 EXPORTS = ("mlp_workspace_bytes", "mlp_init", "mlp_set_stream", "mlp_strategy_workspace_bytes",
            "mlp_set_strategy", "mlp_forward", "mlp_backward",
            "mlp_sgd_step", "mlp_train_epochs", "mlp_check_errors", "mlp_profile",
-           "mlp_last_kernel_ms", "mlp_launch_info", "mlp_destroy", "mlp_status_string",
+           "mlp_last_kernel_ms", "mlp_launch_info", "mlp_phase_cycles", "mlp_destroy",
+           "mlp_status_string",
            "mlp_deep_param_count", "mlp_deep_workspace_bytes", "mlp_deep_init", "mlp_deep_forward",
            "mlp_deep_backward", "mlp_deep_sgd_step", "mlp_deep_train_epochs",
            "mlp_deep_check_errors", "mlp_deep_profile", "mlp_deep_last_kernel_ms",
@@ -84,6 +85,7 @@ def load(require_built: bool = True):
         "mlp_last_kernel_ms": (ctypes.c_int, [_vp, ctypes.POINTER(_f32)]),
         "mlp_launch_info": (ctypes.c_int, [_vp, _i64, _i64, _i32, ctypes.POINTER(_i32),
                                            ctypes.POINTER(_i64)]),
+        "mlp_phase_cycles": (ctypes.c_int, [_vp, _vp, _i64, ctypes.POINTER(_i64)]),
         "mlp_destroy": (None, [_vp]),
         "mlp_status_string": (ctypes.c_char_p, [ctypes.c_int]),
         "mlp_deep_param_count": (_i64, [_i32, _i32, _i32]),
@@ -270,6 +272,27 @@ def mlp_launch_info(ctx: Context, n, batch, epochs):
     _check("mlp_launch_info", load().mlp_launch_info(ctx.handle, n, batch, epochs,
                                                      ctypes.byref(wg), ctypes.byref(launches)))
     return int(wg.value), int(launches.value)
+
+
+PHASE_NAMES = ("forward operands", "forward", "exchange A wait, tile 0",
+               "backward tile 0 + exchange A wait, tile 1", "backward last tile + P to LDS",
+               "P barrier", "exchange B stores", "exchange B wait", "update + exchange C stores",
+               "owners barrier", "exchange C gather", "step barrier")
+
+
+def mlp_phase_cycles(ctx: Context):
+    """Phase-cycle sums of the context's last fused-trainer call made with
+    MLP_TRACE=1 (see include/mlp.h): an int64 array [workgroups, 2, 16], or None
+    when no traced call wrote any."""
+    import numpy as np
+    words = _i64(0)
+    _check("mlp_phase_cycles", load().mlp_phase_cycles(ctx.handle, None, 0, ctypes.byref(words)))
+    if words.value <= 0:
+        return None
+    out = np.zeros(words.value, dtype=np.uint64)
+    _check("mlp_phase_cycles", load().mlp_phase_cycles(ctx.handle, out.ctypes.data, words.value,
+                                                       ctypes.byref(words)))
+    return out.astype(np.int64).reshape(-1, 2, 16)
 
 
 def mlp_status_string(status: int) -> str:

@@ -587,3 +587,27 @@ def test_divergence_is_flagged(mlp, strategy):
     mlp.mlp_train_epochs(ctx, X, Y, 256, 0.002, 1, perm=P, step_loss=sl)
     mlp.mlp_check_errors(ctx)
     assert np.all(np.isfinite(sl.cpu().numpy()))
+
+
+def test_tag_range_wrap_clears_and_restarts(mlp):
+    """A context whose step tags start 20 below 2^32: the first 10-step call fits,
+    the second would wrap, so the library clears the exchange words and restarts
+    the tags at 1. Both calls give bitwise what a context with fresh tags gives."""
+    n, h, B, lr = 4096, 256, 256, 0.01
+    d = datagen.make_data(n, h, epochs=1, shuffle=True, seed=81)
+    X, Y, P = _to(d.X), _to(d.Y), _to(d.perm)
+    runs = []
+    for base in (None, str(2 ** 32 - 20)):
+        with _env(MLP_TAG_BASE=base):
+            ctx, w1, w2 = _ctx(mlp, d.W1, d.W2, B)
+        out = []
+        for call in range(2):
+            sl = torch.zeros(10, dtype=torch.float32, device="cuda")
+            mlp.mlp_train_epochs(ctx, X, Y, B, lr, 1, perm=P, max_steps=10, step_loss=sl)
+            torch.cuda.synchronize()
+            mlp.mlp_check_errors(ctx)
+            out.append((w1.cpu().numpy(), w2.cpu().numpy(), sl.cpu().numpy()))
+        runs.append(out)
+    for a, b in zip(runs[0], runs[1]):
+        for x, y in zip(a, b):
+            assert np.array_equal(x, y)
