@@ -11,8 +11,10 @@ roofline: algorithmic FLOPs of one launch of the training kernel
 (134 h FLOP per sample, the five contractions of eqs. 11-18 at 2 FLOP per
 multiply-add) divided by that launch's duration, measured with HIP events on
 the library's stream, against MI355X's dense fp32 peak (157.3 TFLOP/s).
-cpu_baseline: the fp64 oracle on the host, single-threaded, on a bounded prefix
-of the same workload (its first steps, same permutation).
+cpu_baseline: the fp64 oracle on the host cores (oracle_mt.c: each batch cut into
+64 fixed row chunks, OpenMP over the chunks, on OMP_NUM_THREADS threads or else
+every core the process may use), on a bounded prefix of the same workload (its
+first steps, same permutation).
 """
 import argparse
 import hashlib
@@ -33,6 +35,7 @@ HBM_PEAK_GBS = 8000.0
 TRAINER_SOURCES = ("paper_2606_30497_amd/csrc/train_persistent.hip",
                    "paper_2606_30497_amd/csrc/api.hip",
                    "paper_2606_30497_amd/csrc/lanes.h",
+                   "paper_2606_30497_amd/csrc/tags.h",
                    "paper_2606_30497_amd/csrc/mlp_internal.h",
                    "include/mlp.h")
 
@@ -61,21 +64,26 @@ def load_traffic(workload_name):
 
 def cpu_baseline(w, data, max_seconds):
     import oracle
-    steps = 1
+    threads = oracle.mt_threads()
     # size the prefix from a one-step probe so the whole leg takes ~max_seconds
     t = time.perf_counter()
-    oracle.train(data.X, data.Y, data.W1, data.W2, w.batch, w.lr, w.epochs, perm=data.perm,
-                 max_steps=1)
+    oracle.mt_train(data.X, data.Y, data.W1, data.W2, w.batch, w.lr, w.epochs, perm=data.perm,
+                    max_steps=1)
     one = time.perf_counter() - t
     steps = max(1, min(w.steps, int(max_seconds / max(one, 1e-6))))
     t = time.perf_counter()
-    oracle.train(data.X, data.Y, data.W1, data.W2, w.batch, w.lr, w.epochs, perm=data.perm,
-                 max_steps=steps)
+    oracle.mt_train(data.X, data.Y, data.W1, data.W2, w.batch, w.lr, w.epochs, perm=data.perm,
+                    max_steps=steps)
     dt = time.perf_counter() - t
     samples = min(steps * w.batch, w.n * w.epochs)
-    return {"value": samples / dt, "unit": "samples/s", "cores": 1, "kind": "oracle",
-            "sample": "first %d SGD steps (%d samples) of the same workload, fp64, one thread"
-                      % (steps, samples)}
+    try:
+        affinity = len(os.sched_getaffinity(0))
+    except AttributeError:
+        affinity = os.cpu_count()
+    return {"value": samples / dt, "unit": "samples/s", "cores": threads, "kind": "oracle",
+            "sample": "first %d SGD steps (%d samples, %.1f%% of the run) of the same workload, "
+                      "fp64, %d threads (%d cores in the process's affinity mask)"
+                      % (steps, samples, 100.0 * samples / (w.n * w.epochs), threads, affinity)}
 
 
 def copy_calibration(mib):
@@ -182,6 +190,49 @@ def measure(w, args, mlp, torch, np, data=None):
     return out
 
 
+def measure_phases(w, args, mlp, torch, np):
+    """Where a fused-trainer SGD step of workload w spends its cycles: one traced
+    call (MLP_TRACE=1) over the first args.phase_steps steps; per phase, the
+    median over workgroups of the cycles per step of compute wave 0 and of the
+    owner wave (mlp_phase_cycles)."""
+    import datagen
+    data = datagen.make_workload(w)
+    dev = torch.device("cuda:0")
+    X = torch.from_numpy(data.X).to(dev)
+    Y = torch.from_numpy(data.Y).to(dev)
+    perm = None if data.perm is None else torch.from_numpy(data.perm).to(dev)
+    W1 = torch.from_numpy(data.W1).to(dev)
+    W2 = torch.from_numpy(data.W2).to(dev)
+    ctx = mlp.mlp_init(W1, W2, w.batch)
+    mlp.mlp_profile(ctx, True)
+    steps = min(args.phase_steps, w.steps)
+    mlp.mlp_train_epochs(ctx, X, Y, w.batch, w.lr, w.epochs, perm=perm, max_steps=steps)  # warm-up
+    W1.copy_(torch.from_numpy(data.W1).to(dev))
+    W2.copy_(torch.from_numpy(data.W2).to(dev))
+    os.environ["MLP_TRACE"] = "1"
+    try:
+        mlp.mlp_train_epochs(ctx, X, Y, w.batch, w.lr, w.epochs, perm=perm, max_steps=steps)
+        ms = mlp.mlp_last_kernel_ms(ctx)
+        ph = mlp.mlp_phase_cycles(ctx)
+    finally:
+        del os.environ["MLP_TRACE"]
+    mlp.mlp_check_errors(ctx)
+    ph = ph[ph[:, 0, 0] > 0].astype(np.float64)
+    per = ph[:, :, 1:13] / ph[:, :, 0:1]                    # cycles per step
+    clock = float(np.median(ph[:, 0, 14] / (ph[:, 0, 13] * 10e-9)))
+    table = {}
+    for i, name in enumerate(mlp.PHASE_NAMES):
+        table[name] = {"wave0_cycles": float(np.median(per[:, 0, i])),
+                       "owner_cycles": float(np.median(per[:, 1, i])),
+                       "wave0_p90": float(np.percentile(per[:, 0, i], 90))}
+    tot = np.median(per.sum(axis=2), axis=0)
+    return {"metric": "cycles per SGD step by phase (median over workgroups)",
+            "config": {"workload": w.name, "steps_traced": steps, "workgroups": int(ph.shape[0])},
+            "clock_hz": clock, "us_per_sgd_step_traced": ms * 1e3 / steps,
+            "total_cycles": {"wave0": float(tot[0]), "owner": float(tot[1])},
+            "phases": table}
+
+
 def measure_forward(h, X, args, mlp, torch, np):
     """mlp_forward over every row of X (resident in HBM) with a 32-h-1 net: rows/s
     and the fraction of the fp32 MFMA peak (66 h FLOP per row: 2*32*h of eq. 11 on
@@ -226,14 +277,16 @@ def measure_forward(h, X, args, mlp, torch, np):
     extra = {}
     if not args.no_cpu_baseline:
         import oracle
-        Xh = X.cpu().numpy() if n <= 200_000 else X[:200_000].cpu().numpy()
-        rows = max(1000, min(Xh.shape[0], int(2e9 / (66.0 * h))))   # about 2 GFLOP of fp64 work
+        threads = oracle.mt_threads()
+        Xh = X[:1_000_000].cpu().numpy()
+        rows = max(1000, min(Xh.shape[0], int(1e10 / (66.0 * h))))   # about 10 GFLOP of fp64 work
         t = time.perf_counter()
-        oracle.forward(Xh[:rows], d.W1, d.W2)
+        oracle.mt_forward(Xh[:rows], d.W1, d.W2)
         dt = time.perf_counter() - t
-        extra["cpu_baseline"] = {"value": rows / dt, "unit": "rows/s", "cores": 1, "kind": "oracle",
-                                 "sample": "oracle forward over the first %d rows, fp64, one thread"
-                                           % rows}
+        extra["cpu_baseline"] = {"value": rows / dt, "unit": "rows/s", "cores": threads,
+                                 "kind": "oracle",
+                                 "sample": "oracle forward over the first %d rows, fp64, %d threads"
+                                           % (rows, threads)}
     return dict({
         "metric": "forward rows/sec (eqs. 11-13 over a resident dataset)",
         "value": n / ((t1 - t0) / args.steps),
@@ -332,6 +385,10 @@ def main():
                     default="fused",
                     help="training strategy (the paper's baseline and optimized strategies, "
                          "the per-step fused tile kernel, or the single-launch trainer)")
+    ap.add_argument("--phases", action="store_true",
+                    help="instead of the headline line: one traced training call of the "
+                         "workload, cycles per SGD step by phase (diagnostic)")
+    ap.add_argument("--phase-steps", type=int, default=2000)
     ap.add_argument("--no-cpu-baseline", action="store_true")
     ap.add_argument("--cpu-seconds", type=float, default=15.0,
                     help="CPU seconds spent on the oracle baseline leg")
@@ -367,6 +424,10 @@ def main():
     if args.suite == "deep":
         for w in datagen.DEEP:
             print(json.dumps(measure_deep(w, args, mlp, torch, np)), flush=True)
+        return
+    if args.phases:
+        print(json.dumps(measure_phases(datagen.WORKLOADS[args.workload], args, mlp, torch, np)),
+              flush=True)
         return
     suite = datagen.SUITES[args.suite] if args.suite else [datagen.WORKLOADS[args.workload]]
     for w in suite:
