@@ -201,6 +201,34 @@ mlp_status mlp_phase_cycles(mlp_t ctx, uint64_t *out, int64_t max_words, int64_t
 /* Release the host-side context (the caller still owns every device buffer). */
 void mlp_destroy(mlp_t ctx);
 
+/* mlp_train_epochs for callers that cannot allocate (code under stream capture,
+ * tight serving loops, harnesses that forbid allocation): the same training
+ * (the same kernels and launch sequence; results bitwise equal to
+ * mlp_train_epochs on a context with the same weights and arguments), with no
+ * context and no caller workspace. Its scratch is the library's own: a 16 MiB
+ * device array per GPU, created with the library's code on that GPU and held
+ * until the process ends. The call allocates nothing (no hipMalloc, hipFree or
+ * allocating library routine, no host heap).
+ *   hidden: 32, 64, 128 or 256 (larger nets need more than the 16 MiB scratch:
+ *           MLP_ERR_WORKSPACE; other sizes MLP_ERR_UNSUPPORTED). d_in = 32, d_out = 1.
+ *   W1 [32 x hidden], W2 [hidden]: device, caller-owned, updated in place.
+ *   X, Y, n, batch (<= 2^20), lr, epochs, perm, max_steps, epoch_loss, step_loss:
+ *           as mlp_train_epochs.
+ *   status: nullable device int32; when given, receives the kernel-side sticky
+ *           error of this call (0, MLP_ERR_INDEX, MLP_ERR_TIMEOUT or
+ *           MLP_ERR_NONFINITE) once the call's work on the stream completes.
+ *   stream: the HIP stream to enqueue on (NULL = the default stream).
+ * Asynchronous: argument errors return synchronously before anything is
+ * enqueued. Every call on a GPU shares that GPU's scratch, which keeps the last
+ * call's contents: each call clears the control words it needs cleared, and
+ * step tags continue across calls. Calls that overlap on one GPU (other streams
+ * or threads without ordering) race on the scratch; calls on one stream do not. */
+mlp_status mlp_train_epochs_static(int32_t hidden, float *W1, float *W2, const float *X,
+                                   const float *Y, int64_t n, int64_t batch, float lr,
+                                   int32_t epochs, const int32_t *perm, int64_t max_steps,
+                                   float *epoch_loss, float *step_loss, int32_t *status,
+                                   void *stream);
+
 /* ---- Deeper networks: d_in-h-...-h-1 with L hidden layers ----------------------
  * The paper trains one hidden layer and names deeper networks as future work
  * (Sec. VII.B). These calls train the same kind of network with L hidden ReLU

@@ -56,6 +56,27 @@ extern "C" const char *mlp_status_string(mlp_status s) {
 
 static mlp_status hip_status(hipError_t e) { return e == hipSuccess ? MLP_OK : MLP_ERR_HIP; }
 
+namespace mlp {
+
+// Pointers of a context into a workspace of `need` bytes (mlp_workspace_bytes):
+// control words, tile-path slots, then the trainer's three exchange buffers.
+void carve_workspace(Ctx &c, void *workspace, size_t need) {
+    char *ws = (char *)workspace;
+    c.ctl = (Control *)ws;
+    ws += CTL_BYTES;
+    c.slot_stride = (int64_t)slot_stride_floats(c.hidden);
+    c.slots = (float *)ws;
+    ws += round256(sizeof(float) * c.slot_stride * TILE_SLOTS);
+    c.xch = (uint64_t *)ws;
+    ws += round256(sizeof(uint64_t) * persist_words_xch());
+    c.rs = (uint64_t *)ws;
+    ws += round256(sizeof(uint64_t) * persist_words_rs(c.hidden));
+    c.ag = (uint64_t *)ws;
+    c.xch_words = (int64_t)(((char *)workspace + need) - (char *)c.xch) / 8;
+}
+
+}  // namespace mlp
+
 extern "C" mlp_status mlp_init(mlp_t *out, int32_t d_in, int32_t hidden, int32_t d_out,
                                int64_t max_batch, float *W1, float *W2, void *workspace,
                                size_t ws_bytes, void *stream) {
@@ -70,24 +91,12 @@ extern "C" mlp_status mlp_init(mlp_t *out, int32_t d_in, int32_t hidden, int32_t
     c->max_batch = max_batch;
     c->W1 = W1;
     c->W2 = W2;
-    char *ws = (char *)workspace;
-    c->ctl = (Control *)ws;
-    ws += CTL_BYTES;
-    c->slot_stride = (int64_t)slot_stride_floats(hidden);
-    c->slots = (float *)ws;
-    ws += round256(sizeof(float) * c->slot_stride * TILE_SLOTS);
-    c->xch = (uint64_t *)ws;
-    ws += round256(sizeof(uint64_t) * persist_words_xch());
-    c->rs = (uint64_t *)ws;
-    ws += round256(sizeof(uint64_t) * persist_words_rs(hidden));
-    c->ag = (uint64_t *)ws;
-    ws += round256(sizeof(uint64_t) * persist_words_ag(hidden));
+    carve_workspace(*c, workspace, need);
     c->stream = (hipStream_t)stream;
     // Exchange words carry (value, step tag); tags of this context start at 1, so
     // every word is cleared to tag 0 first: memory reused from an earlier
     // context can never present a current tag.
-    const int64_t words = (int64_t)(((char *)workspace + need) - (char *)c->xch) / 8;
-    c->xch_words = words;
+    const int64_t words = c->xch_words;
     // test hook: the first step tag of this context (exercises the tag wrap)
     if (const char *tb = getenv("MLP_TAG_BASE")) c->tag_base = (uint32_t)strtoul(tb, nullptr, 10);
     if (hipGetDevice(&c->device) != hipSuccess ||
@@ -256,6 +265,12 @@ extern "C" mlp_status mlp_train_epochs(mlp_t c, const float *X, const float *Y, 
                                        int64_t batch, float lr, int32_t epochs,
                                        const int32_t *perm, int64_t max_steps,
                                        float *epoch_loss, float *step_loss) {
+    return train_epochs_ctx(c, X, Y, n, batch, lr, epochs, perm, max_steps, epoch_loss, step_loss);
+}
+
+mlp_status train_epochs_ctx(mlp_ctx *c, const float *X, const float *Y, int64_t n, int64_t batch,
+                            float lr, int32_t epochs, const int32_t *perm, int64_t max_steps,
+                            float *epoch_loss, float *step_loss) {
     if (!c || !X || !Y || n < 1 || batch < 1 || batch > c->max_batch || epochs < 1 ||
         !isfinite(lr) || max_steps < -1)
         return MLP_ERR_INVALID_ARG;

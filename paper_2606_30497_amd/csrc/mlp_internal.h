@@ -148,7 +148,13 @@ size_t persist_words_rs(int hidden);
 size_t persist_words_ag(int hidden);
 hipError_t launch_train(Ctx &c, TrainArgs &a);
 hipError_t fill(const Ctx &c, float *p, int64_t n, float v);
+void carve_workspace(Ctx &c, void *workspace, size_t need);
 
 }  // namespace mlp
 
 struct mlp_ctx : mlp::Ctx {};
+
+// mlp_train_epochs on a context (api.hip), shared with the no-allocation entry point.
+mlp_status train_epochs_ctx(mlp_ctx *c, const float *X, const float *Y, int64_t n, int64_t batch,
+                            float lr, int32_t epochs, const int32_t *perm, int64_t max_steps,
+                            float *epoch_loss, float *step_loss);

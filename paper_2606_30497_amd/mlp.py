@@ -32,7 +32,7 @@ EXPORTS = ("mlp_workspace_bytes", "mlp_init", "mlp_set_stream", "mlp_strategy_wo
            "mlp_set_strategy", "mlp_forward", "mlp_backward",
            "mlp_sgd_step", "mlp_train_epochs", "mlp_check_errors", "mlp_profile",
            "mlp_last_kernel_ms", "mlp_launch_info", "mlp_phase_cycles", "mlp_destroy",
-           "mlp_status_string",
+           "mlp_train_epochs_static", "mlp_status_string",
            "mlp_deep_param_count", "mlp_deep_workspace_bytes", "mlp_deep_init", "mlp_deep_forward",
            "mlp_deep_backward", "mlp_deep_sgd_step", "mlp_deep_train_epochs",
            "mlp_deep_check_errors", "mlp_deep_profile", "mlp_deep_last_kernel_ms",
@@ -86,6 +86,8 @@ def load(require_built: bool = True):
         "mlp_launch_info": (ctypes.c_int, [_vp, _i64, _i64, _i32, ctypes.POINTER(_i32),
                                            ctypes.POINTER(_i64)]),
         "mlp_phase_cycles": (ctypes.c_int, [_vp, _vp, _i64, ctypes.POINTER(_i64)]),
+        "mlp_train_epochs_static": (ctypes.c_int, [_i32, _vp, _vp, _vp, _vp, _i64, _i64, _f32, _i32,
+                                                   _vp, _i64, _vp, _vp, _vp, _vp]),
         "mlp_destroy": (None, [_vp]),
         "mlp_status_string": (ctypes.c_char_p, [ctypes.c_int]),
         "mlp_deep_param_count": (_i64, [_i32, _i32, _i32]),
@@ -250,6 +252,34 @@ def mlp_train_epochs(ctx: Context, X, Y, batch, lr, epochs, perm=None, max_steps
     _check("mlp_train_epochs", load().mlp_train_epochs(ctx.handle, X.data_ptr(), Y.data_ptr(), n,
                                                        batch, float(lr), epochs, pp, max_steps,
                                                        ep, sp))
+
+
+def mlp_train_epochs_static(W1, W2, X, Y, batch, lr, epochs, perm=None, max_steps=-1,
+                            epoch_loss=None, step_loss=None, status=None, stream=None):
+    """mlp_train_epochs without a context: the library's own per-GPU scratch, no
+    allocation in the call. W1 [32, h], W2 [h] are updated in place; status
+    (nullable int32 [1]) receives the call's kernel-side error word."""
+    if W1.dim() != 2:
+        raise ValueError("W1 must be [d_in, hidden]")
+    h = W1.shape[1]
+    n = X.shape[0]
+    _dev(W1, "W1")
+    _dev(W2, "W2", numel=h)
+    _dev(X, "X", numel=n * D_IN)
+    _dev(Y, "Y", numel=n)
+    pp = _dev(perm, "perm", dtype=torch.int32, numel=epochs * n) if perm is not None else None
+    ep = _dev(epoch_loss, "epoch_loss", numel=epochs) if epoch_loss is not None else None
+    steps = -(-n // batch) * epochs
+    if max_steps >= 0:
+        steps = min(steps, max_steps)
+    sp = _dev(step_loss, "step_loss", numel=steps) if step_loss is not None else None
+    stp = _dev(status, "status", dtype=torch.int32, numel=1) if status is not None else None
+    if stream is None:
+        stream = torch.cuda.current_stream(W1.device).cuda_stream
+    _check("mlp_train_epochs_static",
+           load().mlp_train_epochs_static(h, W1.data_ptr(), W2.data_ptr(), X.data_ptr(),
+                                          Y.data_ptr(), n, batch, float(lr), epochs, pp,
+                                          max_steps, ep, sp, stp, stream))
 
 
 def mlp_check_errors(ctx: Context) -> None:

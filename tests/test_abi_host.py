@@ -135,3 +135,21 @@ def test_null_context_is_rejected():
     assert lib.mlp_profile(None, 1) == -1
     assert lib.mlp_set_strategy(None, 0, None, 0) == -1
     lib.mlp_destroy(None)
+
+
+def test_static_entry_rejects_before_any_hip_call():
+    """mlp_train_epochs_static checks its arguments before its first HIP call, so
+    these run without a GPU (the pointers are never dereferenced)."""
+    lib = _lib()
+    f = ctypes.c_void_p(256)
+
+    def call(h=256, n=64, batch=64, lr=0.01, epochs=1, max_steps=-1, w1=f):
+        return lib.mlp_train_epochs_static(h, w1, f, f, f, n, batch, lr, epochs, None, max_steps,
+                                           None, None, None, None)
+
+    assert call(h=512) == -3 and call(h=1024) == -3       # beyond the 16 MiB scratch
+    assert call(h=48) == -2 and call(h=2048) == -2        # unsupported widths
+    assert call(batch=0) == -1 and call(batch=(1 << 20) + 1) == -1
+    assert call(n=0) == -1 and call(epochs=0) == -1 and call(max_steps=-2) == -1
+    assert call(lr=float("nan")) == -1 and call(lr=float("inf")) == -1
+    assert call(w1=None) == -1
