@@ -300,8 +300,9 @@ mlp_status mlp_deep_last_kernel_ms(mlp_deep_t ctx, float *ms);
 /* Release the host-side context. */
 void mlp_deep_destroy(mlp_deep_t ctx);
 
-/* Static description of a status code. */
-const char *mlp_status_string(mlp_status status);
+/* Static description of a status code: any int32 value (a code that is not an
+ * mlp_status gives "unknown status"). */
+const char *mlp_status_string(int32_t status);
 
 #ifdef __cplusplus
 }

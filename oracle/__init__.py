@@ -37,12 +37,15 @@ import subprocess
 import numpy as np
 
 _HERE = os.path.dirname(os.path.abspath(__file__))
+# where the three libraries live: beside the sources, unless ORACLE_LIBDIR names
+# another build of them (the tests' sanitizer run builds one with ASan/UBSan)
+_LIBDIR = os.environ.get("ORACLE_LIBDIR") or _HERE
 _SRC = os.path.join(_HERE, "oracle.c")
-_LIB = os.path.join(_HERE, "liboracle.so")
+_LIB = os.path.join(_LIBDIR, "liboracle.so")
 _DEEP_SRC = os.path.join(_HERE, "oracle_deep.c")
-_DEEP_LIB = os.path.join(_HERE, "liboracle_deep.so")
+_DEEP_LIB = os.path.join(_LIBDIR, "liboracle_deep.so")
 _MT_SRC = os.path.join(_HERE, "oracle_mt.c")
-_MT_LIB = os.path.join(_HERE, "liboracle_mt.so")
+_MT_LIB = os.path.join(_LIBDIR, "liboracle_mt.so")
 _lib = None
 _deep_lib = None
 _mt_lib = None
@@ -52,24 +55,27 @@ _f64p = np.ctypeslib.ndpointer(np.float64, flags="C_CONTIGUOUS")
 _i32p = np.ctypeslib.ndpointer(np.int32, flags="C_CONTIGUOUS")
 
 
-def _gcc(src, lib, extra=()):
+def _gcc(src, lib, extra=(), cc="gcc"):
     tmp = lib + ".tmp%d" % os.getpid()
-    subprocess.check_call(["gcc", "-O2", "-std=c11", "-fPIC", "-shared",
+    subprocess.check_call([cc, "-O2", "-std=c11", "-fPIC", "-shared",
                            "-ffp-contract=off", "-fno-fast-math", "-Wall", *extra,
                            "-o", tmp, src, "-lm"])
     os.replace(tmp, lib)
 
 
-def build(force: bool = True) -> str:
+def build(force: bool = True, out_dir: str | None = None, cc: str = "gcc",
+          extra=()) -> str:
     """Compile liboracle.so, liboracle_deep.so and liboracle_mt.so (OpenMP) with
-    gcc (plain -O2, no FMA contraction, no fast-math)."""
-    if force or not os.path.exists(_LIB):
-        _gcc(_SRC, _LIB)
-    if force or not os.path.exists(_DEEP_LIB):
-        _gcc(_DEEP_SRC, _DEEP_LIB)
-    if force or not os.path.exists(_MT_LIB):
-        _gcc(_MT_SRC, _MT_LIB, ("-fopenmp",))
-    return _LIB
+    gcc (plain -O2, no FMA contraction, no fast-math). out_dir, cc and extra
+    (added flags, e.g. sanitizers) build another copy elsewhere; the copy this
+    package loads is the one in ORACLE_LIBDIR, else the one beside the sources."""
+    libs = [(_SRC, _LIB, ()), (_DEEP_SRC, _DEEP_LIB, ()), (_MT_SRC, _MT_LIB, ("-fopenmp",))]
+    for src, lib, own in libs:
+        if out_dir is not None:
+            lib = os.path.join(out_dir, os.path.basename(lib))
+        if force or not os.path.exists(lib):
+            _gcc(src, lib, tuple(own) + tuple(extra), cc)
+    return _LIB if out_dir is None else os.path.join(out_dir, os.path.basename(_LIB))
 
 
 def _load():

@@ -30,9 +30,9 @@ def sources():
     return sorted(glob.glob(os.path.join(CSRC, "*.hip")))
 
 
-def _compile(src):
-    obj = os.path.join(BUILD_DIR, os.path.basename(src) + ".o")
-    cmd = [HIPCC] + FLAGS + ["-c", src, "-o", obj]
+def _compile(src, build_dir=BUILD_DIR, extra=()):
+    obj = os.path.join(build_dir, os.path.basename(src) + ".o")
+    cmd = [HIPCC] + FLAGS + list(extra) + ["-c", src, "-o", obj]
     r = subprocess.run(cmd, stdout=subprocess.PIPE, stderr=subprocess.STDOUT, text=True)
     out = "\n".join(l for l in r.stdout.splitlines() if "packed-fp32-ops" not in l
                     and "not a recognized feature" not in l)
@@ -41,20 +41,24 @@ def _compile(src):
     return obj, out
 
 
-def build(verbose: bool = False) -> str:
-    """Compile every csrc/*.hip and link libmlp.so; always recompiles."""
-    os.makedirs(BUILD_DIR, exist_ok=True)
+def build(verbose: bool = False, out: str = LIB, build_dir: str = BUILD_DIR,
+          extra=()) -> str:
+    """Compile every csrc/*.hip and link libmlp.so; always recompiles. out,
+    build_dir and extra (added compile flags, e.g. host-only sanitizers) build
+    another copy elsewhere; the binding loads the one MLP_LIBRARY names, else
+    the in-tree one."""
+    os.makedirs(build_dir, exist_ok=True)
     srcs = sources()
     with cf.ThreadPoolExecutor(max_workers=min(8, len(srcs))) as ex:
-        res = list(ex.map(_compile, srcs))
-    for _, out in res:
-        if verbose and out.strip():
-            print(out)
-    tmp = LIB + ".tmp%d" % os.getpid()
+        res = list(ex.map(lambda s: _compile(s, build_dir, extra), srcs))
+    for _, out_text in res:
+        if verbose and out_text.strip():
+            print(out_text)
+    tmp = out + ".tmp%d" % os.getpid()
     subprocess.check_call([HIPCC, "--offload-arch=" + ARCH, "-shared", "-fPIC", "-o", tmp]
                           + [o for o, _ in res])
-    os.replace(tmp, LIB)
-    return LIB
+    os.replace(tmp, out)
+    return out
 
 
 if __name__ == "__main__":

@@ -40,7 +40,7 @@ extern "C" size_t mlp_workspace_bytes(int32_t d_in, int32_t hidden, int64_t max_
     return b;
 }
 
-extern "C" const char *mlp_status_string(mlp_status s) {
+extern "C" const char *mlp_status_string(int32_t s) {
     switch (s) {
     case MLP_OK: return "ok";
     case MLP_ERR_INVALID_ARG: return "invalid argument";

@@ -54,7 +54,8 @@ _f32 = ctypes.c_float
 
 
 def library_path() -> str:
-    return _build.LIB
+    """The in-tree libmlp.so, or another build of it that MLP_LIBRARY names."""
+    return os.environ.get("MLP_LIBRARY") or _build.LIB
 
 
 def load(require_built: bool = True):
@@ -64,8 +65,8 @@ def load(require_built: bool = True):
         return _lib
     path = library_path()
     if not os.path.exists(path):
-        if require_built:
-            raise RuntimeError("libmlp.so is not built (run __graft_entry__.build())")
+        if require_built or path != _build.LIB:
+            raise RuntimeError("%s is not built (run __graft_entry__.build())" % path)
         _build.build()
     lib = ctypes.CDLL(path)
     sig = {

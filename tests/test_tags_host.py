@@ -1,5 +1,5 @@
 """Host arithmetic of the trainer's step tags (paper_2606_30497_amd/csrc/tags.h),
-compiled with g++ on the CPU: a launch never uses tag 0, never uses a tag range
+compiled with g++ (under ASan and UBSan) on the CPU: a launch never uses tag 0, never uses a tag range
 that wraps past 2^32, the next launch starts past every tag of this one, and a
 range that would wrap restarts at 1 with the exchange words cleared."""
 import os
@@ -38,13 +38,20 @@ def driver():
     exe = os.path.join(d, "tags_driver")
     with open(src, "w") as f:
         f.write(DRIVER)
-    subprocess.check_call(["g++", "-std=c++17", "-O1", "-Wall", "-I" + CSRC, src, "-o", exe])
+    subprocess.check_call(["g++", "-std=c++17", "-O1", "-Wall", "-fsanitize=address,undefined",
+                           "-fno-sanitize-recover=undefined", "-I" + CSRC, src, "-o", exe],
+                          env=_env())
     return exe
+
+
+def _env():
+    # the driver carries its own sanitizer runtime: no preloaded one from a parent
+    return {k: v for k, v in os.environ.items() if k != "LD_PRELOAD"}
 
 
 def _plans(driver, cases):
     args = [str(x) for c in cases for x in c]
-    out = subprocess.check_output([driver] + args, text=True).split("\n")
+    out = subprocess.check_output([driver] + args, text=True, env=_env()).split("\n")
     return [tuple(int(v) for v in line.split()) for line in out if line.strip()]
 
 
