@@ -10,9 +10,8 @@
 // waves that gather the rows of later steps through the epoch permutation (one
 // loader wave alone is limited by how fast it can issue the gathers).
 // One SGD step is:
-//   1. Z1 = X W1 on fp32 MFMA (16x16x4) from the rows staged in LDS; ReLU mask
-//      bits and the partial Ypred over the group's units stay in registers
-//      (eqs. 11-13);
+//   1. Z1 = X W1 on MFMA from the rows staged in LDS; ReLU mask bits and the
+//      partial Ypred over the group's units stay in registers (eqs. 11-13);
 //   2. exchange A (across XCDs, PX-way): each wave sums the PX partial Ypred of
 //      its rows in group order -> Ypred, residual, dZ2 = (2/n_b) r (eqs. 14-15);
 //   3. P = X^T (dZ2 (.) [Z1 > 0]) on MFMA over the wave's rows; the wave
@@ -25,7 +24,22 @@
 //   5. exchange C (inside the XCD, all-gather): every workgroup loads the
 //      updated slice into LDS (the second barrier publishes it, together with the
 //      next step's rows).
-// Exchanges use 64-bit words holding (fp32 value, 32-bit step tag). Writers
+// Both contractions are fp32 products computed on bf16 MFMA (16x16x32; 16x16x16
+// for the backward of 16-row waves): every fp32 operand x is split into three
+// bf16 parts x = x0 + x1 + x2 (each part the bf16 rounding of what the previous
+// ones leave: |x1| <= 2^-8 |x|, |x2| <= 2^-16 |x|, and the three sum to x
+// exactly while no part underflows), and of the nine part products the six
+// with i + j <= 2 are accumulated in fp32, smallest first. The three dropped
+// ones stay below about 2^-23 |a b| together (twice fp32's unit roundoff), so
+// each product keeps fp32 accuracy, in about 2.5 times fewer MFMA cycles than
+// on fp32 MFMA
+// (8192 multiply-adds: six 16x16x32 bf16 MFMAs of about 17 cycles, against
+// eight 16x16x4 fp32 ones of 32). bf16 MFMAs also leave the SIMD to the other
+// waves (fp32 MFMAs hold off their issue). The loader waves split the rows they
+// stage; the owners split the weights they update and publish the parts.
+// Exchanges use 64-bit words holding (32-bit payload, 32-bit step tag): an fp32
+// value, or, for the W1 words of exchange C, one bf16 part of two adjacent
+// inputs. Writers
 // never wait; readers load their words directly and reload any word whose tag
 // is not yet current. Every sum runs in a fixed order, so results are bitwise
 // reproducible and identical in every group that computes them. No
@@ -81,20 +95,24 @@ struct Shape {
     static constexpr int LPS = PR / SG;                    // sources per owner lane
     static_assert(KP % 16 == 0 && KPW * NWO == KP && NWO >= 1 && NWO <= NCW && KPW <= 64 &&
                       PR % SG == 0 && (SG == 1 || SG == 2 || SG == 4), "ownership");
-    static constexpr int XS = 36;                          // X tile row stride (floats)
-    static constexpr int WS = 36;                          // weight slice row stride
+    static constexpr int XRS = 40;                         // bf16 row stride of a staged X part
+    static constexpr int WPS = 40;                         // bf16 row stride of a W1 part (per unit)
+    static constexpr int CW = 49 * U;                      // exchange-C words per group: [3][U][16] + [U]
+    static constexpr int NPW = 3 * U / 32;                 // exchange-C word pairs per compute thread
+    static constexpr int CHC = NPW <= 8 ? NPW : (NPW % 8 == 0 ? 8 : 6);   // of them in flight at once
     static constexpr int PS = 36;                          // P partial row stride (per unit, k inner)
     static constexpr int RSW = 32 * U;                     // exchange-B words per workgroup
     static constexpr int GBW = (PR * RSW + PR + 31) / 32 * 32;   // exchange-B words per group
     static constexpr int RPL = R / (8 * NLW);              // rows per loader lane
-    // LDS carve-up, in floats
-    static constexpr int O_X = 0;                          // [2][R][XS] staged rows
-    static constexpr int O_Y = O_X + 2 * R * XS;           // [2][R]
-    static constexpr int O_YP = O_Y + 2 * R;               // [WU][R] partial Ypred
-    static constexpr int O_P = O_YP + WU * R;              // [WR][U][PS] P partials
-    static constexpr int O_WSL = O_P + WR * U * PS;        // [U][WS] weight slice
-    static constexpr int O_SSE = O_WSL + U * WS;           // [NCW]
-    static constexpr int LDS_FLOATS = O_SSE + NCW;
+    // LDS carve-up, in bytes
+    static constexpr int B_XR = 0;                               // [2][3][R][XRS] bf16: staged rows, split
+    static constexpr int B_WP = B_XR + 2 * 3 * R * XRS * 2;      // [3][U][WPS] bf16: W1 slice, split
+    static constexpr int B_W2 = B_WP + 3 * U * WPS * 2;          // [U] float: W2 slice
+    static constexpr int B_Y = B_W2 + U * 4;                     // [2][R] float
+    static constexpr int B_YP = B_Y + 2 * R * 4;                 // [WU][R] partial Ypred
+    static constexpr int B_P = B_YP + WU * R * 4;                // [WR][U][PS] P partials
+    static constexpr int B_SSE = B_P + WR * U * PS * 4;          // [NCW]
+    static constexpr int LDS_BYTES = B_SSE + NCW * 4;
 
     static_assert(R % 16 == 0 && U % 16 == 0, "tiles");
     static_assert(WR * WU == NCW && NR % WR == 0 && NU % WU == 0, "wave split");
@@ -105,7 +123,10 @@ struct Shape {
     static_assert(R <= RMAX && R <= 128, "rows");
     static_assert(PX == 1 || PX == 2 || PX == 4 || PX == 8, "groups");
     static_assert(PR >= 1 && PR <= 32, "workgroups per group");
-    static_assert(O_WSL % 4 == 0 && O_P % 4 == 0, "float4 alignment");
+    static_assert(B_WP % 16 == 0 && B_W2 % 16 == 0 && B_P % 16 == 0, "LDS alignment");
+    static_assert(NPW * 256 * 2 == 48 * U && NPW % CHC == 0 && U / 2 <= 256, "exchange-C pairs");
+    static_assert(LDS_BYTES <= 160 * 1024, "LDS");
+    static_assert(RTW == 1 || RTW == 2, "backward K blocks");
 };
 
 // ---------------------------------------------------------------------------
@@ -182,6 +203,58 @@ __device__ __forceinline__ void wave_sync() {
     __builtin_amdgcn_fence(__ATOMIC_ACQUIRE, "wavefront");
 }
 
+// ---- fp32 products on bf16 MFMA ----------------------------------------------
+typedef uint32_t u2v __attribute__((ext_vector_type(2)));
+typedef uint32_t u4v __attribute__((ext_vector_type(4)));
+typedef float f2v __attribute__((ext_vector_type(2)));
+typedef __bf16 bf2v __attribute__((ext_vector_type(2)));
+typedef __bf16 bf8v __attribute__((ext_vector_type(8)));
+typedef short s4v __attribute__((ext_vector_type(4)));
+
+// bf16 roundings (to nearest even) of a and b, packed (a in the low half)
+__device__ __forceinline__ uint32_t bf16x2(float a, float b) {
+    return __builtin_bit_cast(uint32_t, __builtin_convertvector(f2v{a, b}, bf2v));
+}
+__device__ __forceinline__ float lo_f(uint32_t w) { return __uint_as_float(w << 16); }
+__device__ __forceinline__ float hi_f(uint32_t w) { return __uint_as_float(w & 0xFFFF0000u); }
+
+// Three bf16 parts of a pair: a = a0 + a1 + a2, b likewise; part i of both in
+// one word (a in the low half). Each difference below is exact in fp32.
+struct Split3 {
+    uint32_t p[3];
+};
+__device__ __forceinline__ Split3 split3(float a, float b) {
+    Split3 r;
+    r.p[0] = bf16x2(a, b);
+    a -= lo_f(r.p[0]);
+    b -= hi_f(r.p[0]);
+    r.p[1] = bf16x2(a, b);
+    a -= lo_f(r.p[1]);
+    b -= hi_f(r.p[1]);
+    r.p[2] = bf16x2(a, b);
+    return r;
+}
+
+__device__ __forceinline__ f4 mfma_k32(u4v a, u4v b, f4 c) {
+    return __builtin_amdgcn_mfma_f32_16x16x32_bf16(__builtin_bit_cast(bf8v, a),
+                                                   __builtin_bit_cast(bf8v, b), c, 0, 0, 0);
+}
+__device__ __forceinline__ f4 mfma_k16(u2v a, u2v b, f4 c) {
+    return __builtin_amdgcn_mfma_f32_16x16x16bf16_1k(__builtin_bit_cast(s4v, a),
+                                                     __builtin_bit_cast(s4v, b), c, 0, 0, 0);
+}
+// c += A B with both operands in three parts: the products of part orders
+// i + j <= 2, the smallest first
+template <class V, class F>
+__device__ __forceinline__ f4 mfma3(const V (&a)[3], const V (&b)[3], f4 c, F mfma) {
+    c = mfma(a[2], b[0], c);
+    c = mfma(a[1], b[1], c);
+    c = mfma(a[0], b[2], c);
+    c = mfma(a[1], b[0], c);
+    c = mfma(a[0], b[1], c);
+    return mfma(a[0], b[0], c);
+}
+
 // Read a field of the kernel argument block at its use, straight from the
 // kernarg segment: the load is not hoisted to the kernel entry, so arguments
 // needed only off the hot path hold no registers through the step loop.
@@ -238,23 +311,24 @@ struct Waiter {
     }
 };
 
-// C word pairs per thread of the all-gathered weight slice ([unit][33] words;
-// pair i = i0 + 256 q at byte offset base + 16 i) into the LDS slice ([unit][WS]).
-template <int C, int WS>
-__device__ __forceinline__ void gather_slice(Waiter &wt, rsrc_t r, uint32_t base, float *Wsl, int i0,
-                                             uint32_t tag) {
-    W2 w[C];
+// N word pairs per thread of the all-gathered W1 slice (pair i = i0 + 256 q at
+// byte offset base + 16 i): its two words carry part p = i / (8 U) of inputs
+// 4 m .. 4 m + 3 (m = i % 8) of unit (i / 8) % U, as bf16 pairs, and go to LDS
+// in one 8-byte store.
+template <int N, int U, int WPS>
+__device__ __forceinline__ void gather_parts(Waiter &wt, rsrc_t r, uint32_t base, int i0,
+                                             uint32_t tag, uint16_t *WP) {
+    W2 w[N];
     auto reload = [&](int q) { return ld2(r, base + 16u * (uint32_t)(i0 + 256 * q)); };
 #pragma unroll
-    for (int q = 0; q < C; ++q) w[q] = reload(q);
+    for (int q = 0; q < N; ++q) w[q] = reload(q);
     wt.settle(w, tag, reload);
 #pragma unroll
-    for (int q = 0; q < C; ++q) {
-        const int i = 2 * (i0 + 256 * q);
-        const int j0 = i / 33, k0 = i - j0 * 33;
-        const int j1 = (i + 1) / 33, k1 = i + 1 - j1 * 33;
-        Wsl[j0 * WS + k0] = val_of(w[q].a);
-        Wsl[j1 * WS + k1] = val_of(w[q].b);
+    for (int q = 0; q < N; ++q) {
+        const int i = i0 + 256 * q;
+        const int p = i / (8 * U), ul = (i / 8) % U, m = i % 8;
+        *reinterpret_cast<u2v *>(WP + (p * U + ul) * WPS + 4 * m) =
+            u2v{(uint32_t)w[q].a, (uint32_t)w[q].b};
     }
 }
 
@@ -277,9 +351,9 @@ struct Pos {
 //   s_memrealtime ticks (100 MHz) and [14] elapsed core cycles over the summed
 //   steps (their ratio is the clock), [15] 0.
 // Phases: 1 forward operands from LDS (waited for), 2 forward MFMAs, epilogue
-// and exchange-A stores, 3 exchange-A wait of row tile 0, 4 backward of tile 0
-// and exchange-A wait of tile 1, 5 backward of the last tile and the P
-// partials into LDS, 6 P barrier, 7 exchange-B stores, 8 exchange-B wait
+// and exchange-A stores, 3 exchange-A wait of row tile 0, 4 residual of tile 0
+// and exchange-A wait of tile 1, 5 residual of the last tile, the backward and
+// the P partials into LDS, 6 P barrier, 7 exchange-B stores, 8 exchange-B wait
 // (owners), 9 update and exchange-C stores (owners), 10 owners barrier,
 // 11 exchange-C gather, 12 step barrier. A phase a wave does not run counts 0.
 constexpr int PHASE_FROM = 8, PHASE_WORDS = 16;
@@ -308,7 +382,8 @@ __global__ __launch_bounds__(NTHR) void k_train(const TrainArgs a) {
 
     constexpr int R = S::R, U = S::U, PR = S::PR, PX = S::PX, H = S::H;
     constexpr int WR = S::WR, WU = S::WU, NUW = S::NUW, RTW = S::RTW, NRW = S::NRW;
-    constexpr int UPW = S::UPW, NPAIR = S::NPAIR, XS = S::XS, WS = S::WS, PS = S::PS;
+    constexpr int UPW = S::UPW, NPAIR = S::NPAIR, XRS = S::XRS, WPS = S::WPS;
+    constexpr int PS = S::PS;
     const int tid = threadIdx.x;
     const int lane = tid & 63;
     const int wave = __builtin_amdgcn_readfirstlane(tid >> 6);
@@ -367,12 +442,24 @@ __global__ __launch_bounds__(NTHR) void k_train(const TrainArgs a) {
         s_flags[5] = 0;
     }
 
-    float *Xall = lds + S::O_X;     // [2][R][XS]
-    float *Yall = lds + S::O_Y;     // [2][R]
-    float *Ypart = lds + S::O_YP;   // [WU][R]
-    float *Pred = lds + S::O_P;     // [WR][U][PS]
-    float *Wsl = lds + S::O_WSL;    // [U][WS]
-    float *SseW = lds + S::O_SSE;   // [NCW]
+    char *ldsb = reinterpret_cast<char *>(lds);
+    uint16_t *XRall = reinterpret_cast<uint16_t *>(ldsb + S::B_XR);   // [2][3][R][XRS]
+    uint16_t *WP = reinterpret_cast<uint16_t *>(ldsb + S::B_WP);      // [3][U][WPS]
+    float *W2s = reinterpret_cast<float *>(ldsb + S::B_W2);           // [U]
+    float *Yall = reinterpret_cast<float *>(ldsb + S::B_Y);           // [2][R]
+    float *Ypart = reinterpret_cast<float *>(ldsb + S::B_YP);         // [WU][R]
+    float *Pred = reinterpret_cast<float *>(ldsb + S::B_P);           // [WR][U][PS]
+    float *SseW = reinterpret_cast<float *>(ldsb + S::B_SSE);         // [NCW]
+    // a weight-slice value into LDS: W1 (k < 32) in three bf16 parts, W2 as is
+    auto put_w = [&](int j, int k, float v) {
+        if (k < 32) {
+            const Split3 q = split3(v, 0.0f);
+#pragma unroll
+            for (int p = 0; p < 3; ++p) WP[(p * U + j) * WPS + k] = (uint16_t)q.p[p];
+        } else {
+            W2s[j] = v;
+        }
+    };
 
     const int steps = (int)a.steps;
     const int spe = (int)((a.n + a.batch - 1) / a.batch);
@@ -384,16 +471,16 @@ __global__ __launch_bounds__(NTHR) void k_train(const TrainArgs a) {
         for (int i = tid; i < U * 33; i += NTHR) {
             const int jl = i / 33, k = i - jl * 33;
             const int ug = gx * U + jl;
-            Wsl[jl * WS + k] = k < 32 ? COLD(W1)[k * H + ug] : COLD(W2)[ug];
+            put_w(jl, k, k < 32 ? COLD(W1)[k * H + ug] : COLD(W2)[ug]);
         }
         Waiter wt{&s_flags[3], 0, false};
 
         if (wave < NCW) {
             // ================= compute waves =================================
-            // exchange buffers: A [2][PR][PX][RMAX], B [2][PX][GBW], C [2][PX][U*33] words
+            // exchange buffers: A [2][PR][PX][RMAX], B [2][PX][GBW], C [2][PX][CW] words
             const rsrc_t rA = make_rsrc(a.xch, 8u * (uint32_t)(2 * PR * PX * RMAX));
             const rsrc_t rB = make_rsrc(a.rs, 8u * (uint32_t)(2 * PX * S::GBW));
-            const rsrc_t rC = make_rsrc(a.ag, 8u * (uint32_t)(2 * PX * U * 33));
+            const rsrc_t rC = make_rsrc(a.ag, 8u * (uint32_t)(2 * PX * S::CW));
             const int wr = wave % WR, wu = wave / WR;
             constexpr int KPW = S::KPW, SG = S::SG, LPS = S::LPS;
             // the owner waves are the last NWO compute waves (the loader shares SIMD 0
@@ -434,7 +521,7 @@ __global__ __launch_bounds__(NTHR) void k_train(const TrainArgs a) {
                 const int nb = cur.sb == spe - 1 ? tail : batch;
                 const int rc = nb - gb * R;        // rows of this workgroup in the batch (may be <= 0)
                 const float scale = cur.sb == spe - 1 ? scale_tail : scale_full;   // 2 / nb
-                const float *Xb = Xall + par * R * XS;
+                const uint16_t *XRb = XRall + par * 3 * R * XRS;
                 const float *Yb = Yall + par * R;
                 const uint32_t bB = 8u * (uint32_t)((par * PX + gx) * S::GBW);   // group block (bytes)
                 PHASE(0);
@@ -456,16 +543,14 @@ __global__ __launch_bounds__(NTHR) void k_train(const TrainArgs a) {
                 // to exchange A, tile by tile; otherwise they meet in LDS first.
                 constexpr bool DIRECT = WU == 1 && PX > 1;
                 const uint32_t bA = 8u * (uint32_t)((par * PR + gb) * PX * RMAX);
-                float w1b[NUW][8], w2v[NUW];
+                // B operand (read at each use, to bound registers): W1 inputs
+                // 8 lq .. 8 lq + 7 of unit li of unit tile u
+                auto wpart = [&](int u, int p) {
+                    return *reinterpret_cast<const u4v *>(WP + (p * U + (wu + u * WU) * 16 + li) * WPS + 8 * lq);
+                };
+                float w2v[NUW];
 #pragma unroll
-                for (int u = 0; u < NUW; ++u) {
-                    const float *wp = Wsl + ((wu + u * WU) * 16 + li) * WS + 8 * lq;
-                    const float4 a0 = *reinterpret_cast<const float4 *>(wp);
-                    const float4 a1 = *reinterpret_cast<const float4 *>(wp + 4);
-                    w1b[u][0] = a0.x; w1b[u][1] = a0.y; w1b[u][2] = a0.z; w1b[u][3] = a0.w;
-                    w1b[u][4] = a1.x; w1b[u][5] = a1.y; w1b[u][6] = a1.z; w1b[u][7] = a1.w;
-                    w2v[u] = Wsl[((wu + u * WU) * 16 + li) * WS + 32];
-                }
+                for (int u = 0; u < NUW; ++u) w2v[u] = W2s[(wu + u * WU) * 16 + li];
                 if constexpr (TR) {
                     asm volatile("s_waitcnt lgkmcnt(0)" ::: "memory");   // the weight operands
                     PHASE(1);
@@ -474,21 +559,20 @@ __global__ __launch_bounds__(NTHR) void k_train(const TrainArgs a) {
 #pragma unroll
                 for (int i = 0; i < RTW; ++i) {
                     const int tile = wr * RTW + i;
-                    const float *xr = Xb + (tile * 16 + li) * XS + 8 * lq;
-                    const float4 xa = *reinterpret_cast<const float4 *>(xr);
-                    const float4 xb = *reinterpret_cast<const float4 *>(xr + 4);
-                    const float xv[8] = {xa.x, xa.y, xa.z, xa.w, xb.x, xb.y, xb.z, xb.w};
+                    // A operand: row li of the tile, inputs 8 lq .. 8 lq + 7
+                    u4v xq[3];
+#pragma unroll
+                    for (int p = 0; p < 3; ++p)
+                        xq[p] = *reinterpret_cast<const u4v *>(XRb + (p * R + tile * 16 + li) * XRS + 8 * lq);
                     // the target group 0 folds into its exchange-A word, read ahead of
                     // the MFMAs so that the store does not wait on LDS
                     const float yv = (DIRECT && gx == 0) ? Yb[tile * 16 + 4 * lq + (li >> 2)] : 0.0f;
                     f4 acc[NUW];
 #pragma unroll
-                    for (int u = 0; u < NUW; ++u) acc[u] = f4{0.f, 0.f, 0.f, 0.f};
-#pragma unroll
-                    for (int t = 0; t < 8; ++t)
-#pragma unroll
-                        for (int u = 0; u < NUW; ++u)
-                            acc[u] = __builtin_amdgcn_mfma_f32_16x16x4f32(xv[t], w1b[u][t], acc[u], 0, 0, 0);
+                    for (int u = 0; u < NUW; ++u) {
+                        const u4v wq[3] = {wpart(u, 0), wpart(u, 1), wpart(u, 2)};
+                        acc[u] = mfma3(xq, wq, f4{0.f, 0.f, 0.f, 0.f}, mfma_k32);
+                    }
                     float yp[4] = {0.f, 0.f, 0.f, 0.f};
 #pragma unroll
                     for (int u = 0; u < NUW; ++u)
@@ -546,17 +630,20 @@ __global__ __launch_bounds__(NTHR) void k_train(const TrainArgs a) {
                     for (int i = 0; i < RTW; ++i)
                         wa[i] = ld2(rA, bA + 8u * (uint32_t)(peer * RMAX + (wr * RTW + i) * 16 + 4 * lq + 2 * hh));
                 }
-                // the backward's A operands (X rows 4 lq + v, inputs li and li + 16)
-                // come out of LDS while exchange A is in flight
-                float xt[RTW][4][2];
+                // the backward's A operands (input kt * 16 + li; rows 4 lq .. 4 lq + 3
+                // of each of the wave's row tiles, 16-bit reads) come out of LDS
+                // while exchange A is in flight
+                u2v xtq[2][3][RTW];
 #pragma unroll
-                for (int i = 0; i < RTW; ++i)
+                for (int kt = 0; kt < 2; ++kt)
 #pragma unroll
-                    for (int v = 0; v < 4; ++v) {
-                        const float *xr = Xb + ((wr * RTW + i) * 16 + 4 * lq + v) * XS + li;
-                        xt[i][v][0] = xr[0];
-                        xt[i][v][1] = xr[16];
-                    }
+                    for (int p = 0; p < 3; ++p)
+#pragma unroll
+                        for (int i = 0; i < RTW; ++i) {
+                            const uint16_t *xp = XRb + (p * R + (wr * RTW + i) * 16 + 4 * lq) * XRS + kt * 16 + li;
+                            xtq[kt][p][i] = u2v{(uint32_t)xp[0] | ((uint32_t)xp[XRS] << 16),
+                                                (uint32_t)xp[2 * XRS] | ((uint32_t)xp[3 * XRS] << 16)};
+                        }
                 // deferred loss of the previous step, reduced while exchange A is in
                 // flight: its words are long written, and they stay intact at least
                 // until this workgroup has passed the barrier below (no group-0
@@ -576,12 +663,8 @@ __global__ __launch_bounds__(NTHR) void k_train(const TrainArgs a) {
                         if (el) el[prev.e] = (float)(epoch_sse * (double)COLD(inv_n));
                     }
                 }
-                f4 pacc[2][NUW];
-#pragma unroll
-                for (int kt = 0; kt < 2; ++kt)
-#pragma unroll
-                    for (int u = 0; u < NUW; ++u) pacc[kt][u] = f4{0.f, 0.f, 0.f, 0.f};
                 float r2acc = 0.f;
+                Split3 gq[RTW][2];   // dZ2 of rows 4 lq + v of each row tile, in parts (v = 0,1 | 2,3)
 #pragma unroll
                 for (int i = 0; i < RTW; ++i) {
                     const int tile = wr * RTW + i;
@@ -626,16 +709,44 @@ __global__ __launch_bounds__(NTHR) void k_train(const TrainArgs a) {
                         gv[2] = hh ? g0 : o0;
                         gv[3] = hh ? g1 : o1;
                     }
-                    // ---- 3. backward: P += X_tile^T (dZ2 (.) mask) ----------------
+                    gq[i][0] = split3(gv[0], gv[1]);
+                    gq[i][1] = split3(gv[2], gv[3]);
+                }
+                // ---- 3. backward: P += X^T (dZ2 (.) mask) over the wave's rows ------
+                // K index 8 lq + j (4 lq + j with one row tile): row 4 lq + (j & 3) of
+                // row tile j >> 2, so that both operands hold only the lane's own rows
+                f4 pacc[2][NUW];
 #pragma unroll
-                    for (int v = 0; v < 4; ++v) {
-                        const float xt0 = xt[i][v][0], xt1 = xt[i][v][1];
+                for (int u = 0; u < NUW; ++u) {
+                    // B operand: dZ2 (.) ReLU'(Z1) of the unit li, in parts
+                    uint32_t bm[RTW][2][3];
 #pragma unroll
-                        for (int u = 0; u < NUW; ++u) {
-                            const bool on = (mbits >> ((i * NUW + u) * 4 + v)) & 1u;
-                            const float gm = on ? gv[v] : 0.0f;     // dZ2 (.) ReLU'(Z1)
-                            pacc[0][u] = __builtin_amdgcn_mfma_f32_16x16x4f32(xt0, gm, pacc[0][u], 0, 0, 0);
-                            pacc[1][u] = __builtin_amdgcn_mfma_f32_16x16x4f32(xt1, gm, pacc[1][u], 0, 0, 0);
+                    for (int i = 0; i < RTW; ++i)
+#pragma unroll
+                        for (int h = 0; h < 2; ++h) {
+                            const uint32_t bits = mbits >> ((i * NUW + u) * 4 + 2 * h);
+                            const uint32_t keep = ((bits & 1u) ? 0x0000FFFFu : 0u) | ((bits & 2u) ? 0xFFFF0000u : 0u);
+#pragma unroll
+                            for (int p = 0; p < 3; ++p) bm[i][h][p] = gq[i][h].p[p] & keep;
+                        }
+#pragma unroll
+                    for (int kt = 0; kt < 2; ++kt) {
+                        if constexpr (RTW == 2) {
+                            u4v aq[3], bq[3];
+#pragma unroll
+                            for (int p = 0; p < 3; ++p) {
+                                aq[p] = u4v{xtq[kt][p][0].x, xtq[kt][p][0].y, xtq[kt][p][1].x, xtq[kt][p][1].y};
+                                bq[p] = u4v{bm[0][0][p], bm[0][1][p], bm[1][0][p], bm[1][1][p]};
+                            }
+                            pacc[kt][u] = mfma3(aq, bq, f4{0.f, 0.f, 0.f, 0.f}, mfma_k32);
+                        } else {
+                            u2v aq[3], bq[3];
+#pragma unroll
+                            for (int p = 0; p < 3; ++p) {
+                                aq[p] = xtq[kt][p][0];
+                                bq[p] = u2v{bm[0][0][p], bm[0][1][p]};
+                            }
+                            pacc[kt][u] = mfma3(aq, bq, f4{0.f, 0.f, 0.f, 0.f}, mfma_k16);
                         }
                     }
                 }
@@ -753,10 +864,15 @@ __global__ __launch_bounds__(NTHR) void k_train(const TrainArgs a) {
                         ow1b -= a.lr * dw1b;
                         ow2 -= a.lr * dw2;
                         if (sg == 0) {
-                            const uint32_t cb = 8u * (uint32_t)((par * PX + gx) * U * 33 + (gb * UPW + jl) * 33 + k0);
-                            st1(rC, cb, pack(ow1a, tag), !plain);
-                            st1(rC, cb + 8u, pack(ow1b, tag), !plain);
-                            if (k0 == 0) st1(rC, cb + 8u * 32u, pack(ow2, tag), !plain);
+                            // the pair (k0, k0 + 1) in three bf16 parts, one word each, and W2
+                            const uint32_t cb = 8u * (uint32_t)((par * PX + gx) * S::CW);
+                            const int ul = gb * UPW + jl;
+                            const Split3 q = split3(ow1a, ow1b);
+#pragma unroll
+                            for (int p = 0; p < 3; ++p)
+                                st1(rC, cb + 8u * (uint32_t)((p * U + ul) * 16 + (k0 >> 1)),
+                                    pack(__uint_as_float(q.p[p]), tag), !plain);
+                            if (k0 == 0) st1(rC, cb + 8u * (uint32_t)(48 * U + ul), pack(ow2, tag), !plain);
                         }
                     }
                     PHASE(9);
@@ -771,31 +887,22 @@ __global__ __launch_bounds__(NTHR) void k_train(const TrainArgs a) {
                     if (a.mode == 0) __syncthreads();
                 PHASE(10);
                 if (a.mode == 0) {
-                    // at most CH word pairs per thread in flight, to bound registers
-                    const uint32_t cbase = 8u * (uint32_t)((par * PX + gx) * U * 33);
-                    constexpr int NP = U * 33 / 2, FULL = NP / 256, REST = NP % 256;
-                    constexpr int CH = FULL < 9 ? FULL : 8;
-                    constexpr int NCH = (FULL + CH - 1) / CH;
-                    static_assert((U * 33) % 2 == 0 && FULL >= 1, "slice pairs");
+                    // the W1 parts in chunks of CHC word pairs per thread (to bound
+                    // registers); the W2 words (threads below U / 2) load first
+                    const uint32_t cbase = 8u * (uint32_t)((par * PX + gx) * S::CW);
                     W2 wr1[1] = {W2{pack(0.f, tag), pack(0.f, tag)}};
                     auto reload1 = [&](int) {
-                        return tid < REST ? ld2(rC, cbase + 16u * (uint32_t)(256 * FULL + tid))
-                                          : W2{pack(0.f, tag), pack(0.f, tag)};
+                        return tid < U / 2 ? ld2(rC, cbase + 8u * (uint32_t)(48 * U + 2 * tid))
+                                           : W2{pack(0.f, tag), pack(0.f, tag)};
                     };
-                    if (REST > 0) wr1[0] = reload1(0);
+                    wr1[0] = reload1(0);
 #pragma unroll
-                    for (int c = 0; c < NCH - 1; ++c)
-                        gather_slice<CH, WS>(wt, rC, cbase, Wsl, tid + 256 * CH * c, tag);
-                    gather_slice<FULL - (NCH - 1) * CH, WS>(wt, rC, cbase, Wsl, tid + 256 * CH * (NCH - 1), tag);
-                    if (REST > 0) {
-                        wt.settle(wr1, tag, reload1);
-                        if (tid < REST) {
-                            const int i = 2 * (256 * FULL + tid);
-                            const int j0 = i / 33, q0 = i - j0 * 33;
-                            const int j1 = (i + 1) / 33, q1 = i + 1 - j1 * 33;
-                            Wsl[j0 * WS + q0] = val_of(wr1[0].a);
-                            Wsl[j1 * WS + q1] = val_of(wr1[0].b);
-                        }
+                    for (int c = 0; c < S::NPW / S::CHC; ++c)
+                        gather_parts<S::CHC, U, WPS>(wt, rC, cbase, tid + 256 * S::CHC * c, tag, WP);
+                    wt.settle(wr1, tag, reload1);
+                    if (tid < U / 2) {
+                        W2s[2 * tid] = val_of(wr1[0].a);
+                        W2s[2 * tid + 1] = val_of(wr1[0].b);
                     }
                 }
                 PHASE(11);
@@ -910,13 +1017,17 @@ __global__ __launch_bounds__(NTHR) void k_train(const TrainArgs a) {
                     pfy[j] = y;
                 }
             };
+            // a row's inputs 4 lc .. 4 lc + 3 in three bf16 parts
             auto stage = [&](int buf) {
-                float *Xd = Xall + buf * R * XS;
+                uint16_t *XRd = XRall + buf * 3 * R * XRS;
                 float *Yd = Yall + buf * R;
 #pragma unroll
                 for (int j = 0; j < RPL; ++j) {
                     const int r = lr0 + 8 * NLW * j;
-                    *reinterpret_cast<float4 *>(Xd + r * XS + 4 * lc) = pfx[j];
+                    const Split3 s01 = split3(pfx[j].x, pfx[j].y), s23 = split3(pfx[j].z, pfx[j].w);
+#pragma unroll
+                    for (int p = 0; p < 3; ++p)
+                        *reinterpret_cast<u2v *>(XRd + (p * R + r) * XRS + 4 * lc) = u2v{s01.p[p], s23.p[p]};
                     if (lc == 0) Yd[r] = pfy[j];
                 }
             };
@@ -998,8 +1109,9 @@ static hipError_t launch_shape(hipStream_t stream, TrainArgs &a, bool regular) {
                                       stream);
 }
 
-// Modelled step time (seconds): MFMA work of one wave (forward and backward, 32
-// cycles per 16x16x4 fp32 MFMA at 2.4 GHz), exchange A across XCDs when PX > 1,
+// Modelled step time (seconds): MFMA work of one wave (six bf16 MFMAs of about
+// 17 cycles at 2.4 GHz per fp32 product tile: forward RTW * NUW tiles, backward
+// 2 * NUW), exchange A across XCDs when PX > 1,
 // the rounds of exchanges B and C (each round one load round trip) and the
 // owner's loads per lane. The constants are fitted to step times measured on
 // MI355X (at batch 64 and 256, eight groups of few workgroups beat one group of
@@ -1008,9 +1120,8 @@ template <class S>
 static double shape_cost() {
     constexpr int CHB = S::LPS < 8 ? S::LPS : 8;
     constexpr int rounds_b = S::LPS / CHB;
-    constexpr int NP = S::U * 33 / 2, FULL = NP / 256, CH = FULL < 9 ? FULL : 8;
-    constexpr int rounds_c = (FULL + CH - 1) / CH;
-    const double compute = 32.0 * 16.0 * S::NUW * S::RTW / 2.4e9;
+    constexpr int rounds_c = S::NPW / S::CHC;
+    const double compute = 17.0 * 6.0 * S::NUW * (S::RTW + 2) / 2.4e9;
     return compute + (S::PX > 1 ? 1.5e-6 : 0.0) + 0.6e-6 * rounds_b + 0.05e-6 * S::LPS +
            0.5e-6 * rounds_c;
 }
@@ -1031,7 +1142,7 @@ static TrainPlan plan_of(int inst) {
     p.rmax = RMAX;
     p.rs_stride = S::GBW;
     p.grid = 8 * S::PR;
-    const size_t bytes = sizeof(float) * (size_t)S::LDS_FLOATS;
+    const size_t bytes = (size_t)S::LDS_BYTES;
     const size_t one_per_cu = 84 * 1024;   // > half of the 160 KB LDS: one workgroup per CU
     p.lds = bytes > one_per_cu ? bytes : one_per_cu;
     p.cost = shape_cost<S>();
@@ -1116,7 +1227,8 @@ bool plan_train(int hidden, int64_t batch, TrainPlan *plan) {
 size_t persist_words_xch() { return (size_t)2 * 32 * 8 * RMAX; }
 // two parities x up to 8 groups x (32 workgroups x 32 U words + 32 loss words)
 size_t persist_words_rs(int hidden) { return (size_t)2 * 32 * ((size_t)hidden * 32 + 8 * 32); }
-size_t persist_words_ag(int hidden) { return (size_t)2 * hidden * 33; }
+// two parities x (three bf16-part words per W1 pair of inputs, one W2 word) per unit
+size_t persist_words_ag(int hidden) { return (size_t)2 * hidden * 49; }
 
 hipError_t launch_train(Ctx &c, TrainArgs &a) {
     a.xch = c.xch;

@@ -306,7 +306,7 @@ def mlp_launch_info(ctx: Context, n, batch, epochs):
 
 
 PHASE_NAMES = ("forward operands", "forward", "exchange A wait, tile 0",
-               "backward tile 0 + exchange A wait, tile 1", "backward last tile + P to LDS",
+               "residual tile 0 + exchange A wait, tile 1", "residual + backward + P to LDS",
                "P barrier", "exchange B stores", "exchange B wait", "update + exchange C stores",
                "owners barrier", "exchange C gather", "step barrier")
 
