@@ -289,24 +289,59 @@ struct Waiter {
         if (aborted) *stamp = step + 1;
     }
     // w[i] holds a loaded word (or word pair); reload(i) loads it again. Wait
-    // until every tag is current.
-    template <int N, class T, class Reload>
+    // until every tag is current. With D = 2 two polls are in flight: the next
+    // one is issued before the previous is checked, so a word that lands just
+    // after a poll left is seen half a round trip sooner. Exchanges B and C
+    // (inside an XCD) gain from it; exchange A, whose loads cross XCDs, and
+    // deeper pipelines lose (measured: 32-256-1 at batch 4096, 5.24 -> 4.96 us
+    // per step with B and C at D = 2; three or four polls in flight, 8.9 us).
+    template <int D, int N, class T, class Reload>
     __device__ __forceinline__ void settle(T (&w)[N], uint32_t tag, Reload reload) {
-        uint32_t spins = 0;
-        uint64_t deadline = 0;
-        while (true) {
+        static_assert(D == 1 || D == 2, "polls in flight");
+        auto ok = [&](const T (&x)[N]) {
             uint32_t bad = 0;
 #pragma unroll
-            for (int i = 0; i < N; ++i) bad |= stale(w[i], tag);
-            if (bad == 0 || aborted) break;
-            if (spins == 0) deadline = now_ticks() + COLD(timeout_ticks);
-            if ((++spins & 63u) == 0) {
-                check(deadline);
-                if (aborted) break;
-            }
-            asm volatile("" ::: "memory");   // the reloads are not the loads above
+            for (int i = 0; i < N; ++i) bad |= stale(x[i], tag);
+            return bad == 0;
+        };
+        if (ok(w) || aborted) return;
+        const uint64_t deadline = now_ticks() + COLD(timeout_ticks);
+        uint32_t spins = 0;
+        if constexpr (D == 1) {
+            while (true) {
+                asm volatile("" ::: "memory");   // the reloads are not the loads above
 #pragma unroll
-            for (int i = 0; i < N; ++i) w[i] = reload(i);
+                for (int i = 0; i < N; ++i) w[i] = reload(i);
+                if (ok(w)) break;
+                if ((++spins & 63u) == 0) {
+                    check(deadline);
+                    if (aborted) break;
+                }
+            }
+        } else {
+            T v[N];
+            asm volatile("" ::: "memory");
+#pragma unroll
+            for (int i = 0; i < N; ++i) v[i] = reload(i);
+            while (true) {
+                // w is reissued, then v (the older poll) checked, and the reverse
+                asm volatile("" ::: "memory");
+#pragma unroll
+                for (int i = 0; i < N; ++i) w[i] = reload(i);
+                if (ok(v)) {
+#pragma unroll
+                    for (int i = 0; i < N; ++i) w[i] = v[i];
+                    break;
+                }
+                asm volatile("" ::: "memory");
+#pragma unroll
+                for (int i = 0; i < N; ++i) v[i] = reload(i);
+                if (ok(w)) break;
+                if ((++spins & 31u) == 0) {
+                    check(deadline);
+                    if (aborted) break;
+                }
+            }
         }
     }
 };
@@ -322,7 +357,7 @@ __device__ __forceinline__ void gather_parts(Waiter &wt, rsrc_t r, uint32_t base
     auto reload = [&](int q) { return ld2(r, base + 16u * (uint32_t)(i0 + 256 * q)); };
 #pragma unroll
     for (int q = 0; q < N; ++q) w[q] = reload(q);
-    wt.settle(w, tag, reload);
+    wt.settle<2>(w, tag, reload);
 #pragma unroll
     for (int q = 0; q < N; ++q) {
         const int i = i0 + 256 * q;
@@ -650,7 +685,7 @@ __global__ __launch_bounds__(NTHR) void k_train(const TrainArgs a) {
                 // workgroup can store the next step's words before every owner of
                 // group 0 has this workgroup's exchange-B words)
                 if (lossw && s > 0) {
-                    wt.settle(sw, tag_prev, [&](int) { return lane < PR ? ld1(rB, sse_prev) : pack(0.f, tag_prev); });
+                    wt.settle<1>(sw, tag_prev, [&](int) { return lane < PR ? ld1(rB, sse_prev) : pack(0.f, tag_prev); });
                     const float sse = sum64(lane < PR ? val_of(sw[0]) : 0.0f);
                     if (lane == 0) {
                         flag_nonfinite(sse, COLD(err));
@@ -672,7 +707,7 @@ __global__ __launch_bounds__(NTHR) void k_train(const TrainArgs a) {
                     float y0 = 0.f, y1 = 0.f;
                     if constexpr (PX > 1) {
                         W2 one[1] = {wa[i]};
-                        wt.settle(one, tag, [&](int) {
+                        wt.settle<1>(one, tag, [&](int) {
                             return ld2(rA, bA + 8u * (uint32_t)(peer * RMAX + ra));
                         });
                         y0 = val_of(one[0].a);
@@ -834,7 +869,7 @@ __global__ __launch_bounds__(NTHR) void k_train(const TrainArgs a) {
                         auto reload = [&](int b) { return ld2(rB, ob + 8u * (uint32_t)(b * NPAIR)); };
 #pragma unroll
                         for (int b = 0; b < CHB; ++b) w[b] = reload(b);
-                        wt.settle(w, tag, reload);
+                        wt.settle<2>(w, tag, reload);
 #pragma unroll
                         for (int b = 0; b < CHB; ++b) {
                             p0 += val_of(w[b].a);
@@ -899,7 +934,7 @@ __global__ __launch_bounds__(NTHR) void k_train(const TrainArgs a) {
 #pragma unroll
                     for (int c = 0; c < S::NPW / S::CHC; ++c)
                         gather_parts<S::CHC, U, WPS>(wt, rC, cbase, tid + 256 * S::CHC * c, tag, WP);
-                    wt.settle(wr1, tag, reload1);
+                    wt.settle<2>(wr1, tag, reload1);
                     if (tid < U / 2) {
                         W2s[2 * tid] = val_of(wr1[0].a);
                         W2s[2 * tid + 1] = val_of(wr1[0].b);
@@ -942,7 +977,7 @@ __global__ __launch_bounds__(NTHR) void k_train(const TrainArgs a) {
                                                           (lane < PR ? lane : 0));
                 auto reload = [&](int) { return lane < PR ? ld1(rB, sse_last) : pack(0.f, tag_last); };
                 uint64_t swl[1] = {reload(0)};
-                wt.settle(swl, tag_last, reload);
+                wt.settle<1>(swl, tag_last, reload);
                 const float sse = sum64(lane < PR ? val_of(swl[0]) : 0.0f);
                 if (lane == 0) {
                     flag_nonfinite(sse, COLD(err));
