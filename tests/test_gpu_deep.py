@@ -8,11 +8,16 @@ Two kinds of inputs:
   the ReLU masks cannot differ, so the gradients are held to 1e-5 (only the
   backward's sums round);
 - Gaussian (the evaluation-workload recipe): the forward and the loss are
-  continuous at the ReLU kink and are held to 1e-5; gradients to 1e-3, since an
-  fp32 pre-activation within rounding of zero may take either mask value
-  (a correct result either way) and deep nets have many of them. At L = 1 the
-  network is the paper's and the gradients meet the main path's 1e-4 bar after
-  the kink alignment of tests/parity.py.
+  continuous at the ReLU kink and are held to 1e-5. An fp32 pre-activation
+  within rounding of zero may take either mask value (a correct result either
+  way), so the gradient checks run on the rows of the batch whose every
+  pre-activation is farther from zero than a rigorous bound on the device's
+  rounding error (_kink_free: then the device's masks are the exact ones) and
+  hold them to 1e-5, ten times inside the main path's per-step bar. The bound compounds with
+  depth, so at eight layers no row qualifies and the whole batch is held to
+  1e-3; the 1024-wide large-tile case also keeps its whole batch (its point is
+  the tile shapes of 2100 rows) and the 1e-3 bar. At L = 1 the network is the paper's
+  and the gradients meet 1e-4 after the kink alignment of tests/parity.py.
 """
 import numpy as np
 import pytest
@@ -20,7 +25,7 @@ import torch
 
 import datagen
 import oracle
-from tests.parity import align_kinks, rel
+from tests.parity import U32, align_kinks, rel
 
 pytestmark = pytest.mark.gpu
 
@@ -49,6 +54,30 @@ def _gauss_net(rng, h, L):
         parts.append(rng.standard_normal(K * h) * np.sqrt(2.0 / K))
     parts.append(rng.standard_normal(h) * np.sqrt(2.0 / h))
     return np.concatenate(parts).astype(np.float32)
+
+
+def _kink_free(X, P, h, L, idx):
+    """The rows of idx whose pre-activations all lie farther from zero than a
+    bound on the device's fp32 error. Layer l computes Z = H_{l-1} W_l, a sum of
+    K products, from an input each entry of which is within e_{l-1} of exact
+    (e_0 = 0: X is exact); the device's Z is then within
+    e_l = (K + 2) u sum_k (|H_k| + e_k) |W_kj| + sum_k e_k |W_kj| of exact (the
+    fp32 sum of K terms, each off by at most e_k |W_kj|; ReLU is 1-Lipschitz, so
+    e_l also bounds the layer's output). Where |Z| > e_l the device's ReLU mask
+    equals the exact one."""
+    Ws, _ = oracle.deep_split(np.asarray(P, np.float64), D, h, L)
+    Hp = np.asarray(X, np.float64)[idx]
+    Ep = np.zeros_like(Hp)
+    ok = np.ones(len(idx), bool)
+    for W in Ws:
+        K = W.shape[0]
+        A = np.abs(W)
+        Z = Hp @ W
+        prop = Ep @ A
+        E = (K + 2) * U32 * (np.abs(Hp) @ A + prop) + prop
+        ok &= np.all(np.abs(Z) > E, axis=1)
+        Hp, Ep = np.maximum(Z, 0.0), E
+    return np.ascontiguousarray(idx[ok])
 
 
 def _dyadic(rng, n, h, L):
@@ -117,9 +146,37 @@ def test_gradients_dyadic(mlp, h, L, B):
     assert abs(float(loss.cpu()[0]) - rL) <= 1e-5 * max(rL, 1e-30)
 
 
-@pytest.mark.parametrize("h,L", [(64, 2), (256, 2), (256, 3), (64, 8), (128, 8)])
+@pytest.mark.parametrize("h,L", [(64, 2), (256, 2), (256, 3)])
 @pytest.mark.parametrize("B", [7, 160, 1000])
 def test_gradients_gaussian(mlp, h, L, B):
+    """Loss of a random batch at 1e-5; gradients of a batch of B kink-free rows
+    (drawn from up to 8 B random rows) at 1e-5, as in the dyadic cases (measured
+    0.7-7e-7: with the masks settled only the fp32 sums round)."""
+    rng = np.random.default_rng(h * L + B)
+    d = datagen.make_data(5000, 32, seed=6, with_perm=False)
+    P = _gauss_net(rng, h, L)
+    ctx, _ = _ctx(mlp, P, h, L, 1024)
+    idx = rng.integers(0, 5000, size=B).astype(np.int32)
+    _, loss = mlp.mlp_deep_backward(ctx, _to(d.X), _to(d.Y), _to(idx))
+    _, rL, _ = oracle.deep_grad(d.X, d.Y, P, D, h, L, idx=idx)
+    assert abs(float(loss.cpu()[0]) - rL) <= 1e-5 * rL
+    cand = rng.integers(0, 5000, size=8 * B).astype(np.int32)
+    rows = _kink_free(d.X, P, h, L, cand)[:B]
+    assert len(rows) == B, (len(rows), B)
+    dP, _ = mlp.mlp_deep_backward(ctx, _to(d.X), _to(d.Y), _to(rows))
+    ref, _, _ = oracle.deep_grad(d.X, d.Y, P, D, h, L, idx=rows)
+    e = rel(dP.cpu().numpy(), ref)
+    print("kink-free batch of %d rows: gradient rel %.3e" % (B, e))
+    assert e <= 1e-5
+    mlp.mlp_deep_check_errors(ctx)
+
+
+@pytest.mark.parametrize("h,L", [(64, 8), (128, 8)])
+@pytest.mark.parametrize("B", [7, 160, 1000])
+def test_gradients_gaussian_eight_layers(mlp, h, L, B):
+    """Eight layers: the rounding bound of _kink_free compounds with depth
+    (each layer multiplies it by about sum_k |W_kj|), so no row is provably
+    kink-free; the whole batch is compared at 1e-3, the loss at 1e-5."""
     rng = np.random.default_rng(h * L + B)
     d = datagen.make_data(5000, 32, seed=6, with_perm=False)
     P = _gauss_net(rng, h, L)
