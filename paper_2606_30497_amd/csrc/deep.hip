@@ -29,13 +29,29 @@
 // Every output element is one lane's sum in a fixed order, so results are
 // bitwise reproducible.
 //
-// GEMM tile: 64 x 64 (or 32 x 64, 32 x 32) outputs per workgroup of four waves (each a
-// quarter, as 16 x 16 v_mfma_f32_16x16x4f32 tiles), K in chunks of 32 staged in
-// LDS (operands read along m or n stored k-major with a row stride of TM + 16
-// floats, operands read along k as loaded with a stride of 34, so that MFMA
-// operand reads are conflict-free), alternating between two LDS buffers (one
-// barrier per chunk); the next two chunks' global loads are in flight while the
-// current chunk is computed.
+// GEMM tile: 64 x 64 (or 32 x 64, 32 x 32) outputs per workgroup of four waves
+// (each a quarter, as 16 x 16 MFMA tiles), K in chunks of 32 staged in LDS,
+// alternating between two LDS buffers (one barrier per chunk); the next two
+// chunks' global loads are in flight while the current chunk is computed. Two
+// flavours of the product:
+// - fp32: v_mfma_f32_16x16x4f32 on fp32 operands (in LDS, operands read along
+//   m or n stored k-major with a row stride of TM + 16 floats, operands read
+//   along k as loaded with a stride of 34, so that MFMA operand reads are
+//   conflict-free);
+// - bf16x3: fp32 products formed on the bf16 matrix cores. Each operand is
+//   split once, as it is staged, into three bf16 parts (x = x0 + x1 + x2
+//   exactly, each part the rounding to nearest of what the earlier parts
+//   leave), and a b is the sum of the six part products a_i b_j with
+//   i + j <= 2, each exact in fp32, accumulated by v_mfma_f32_16x16x32_bf16 in
+//   fp32: a0 b0 in one sum, the other five in a second, added at the end. The
+//   dropped part products are below 2.01 u |a b| (u = 2^-24); the second sum's
+//   terms are below 2^-7 |a b| together, so its roundings add about 0.04 K u to
+//   the K u of an fp32 dot product of length K. Six bf16 MFMAs of 16 cycles
+//   replace eight fp32 MFMAs of 32 cycles per 32-deep chunk of a 16 x 16 tile,
+//   and a bf16 MFMA does not hold up the other waves of its SIMD while it runs,
+//   as an fp32 one does; the split costs VALU work and LDS space (the parts as
+//   [3][T][32] bf16, k inner, 16-byte granules permuted by row so that operand
+//   reads and staging writes are conflict-free).
 #include <hip/hip_runtime.h>
 
 #include <math.h>
@@ -51,7 +67,7 @@ namespace mlp {
 
 constexpr int GT = 64;        // GEMM tile (M and N)
 constexpr int GK = 32;        // K chunk
-constexpr int GMS = 34;       // LDS row stride of an x-major operand tile ([x][k], floats)
+constexpr int GMS = 34;       // LDS row stride of an x-major fp32 operand tile ([x][k], floats)
 constexpr int GSTAGES = 2;    // K chunks in flight (register stages; 3 or 4 measured slower)
 constexpr int GEMM_CUS = 256; // compute units the tile choice plans for
 constexpr int SPLIT_MAX = 64; // row chunks of a weight-gradient product
@@ -61,15 +77,44 @@ constexpr int DEEP_MAX_LAYERS = 8;
 enum { OP_NN = 0, OP_TN = 1, OP_NT = 2 };
 enum { EP_NONE = 0, EP_RELU = 1, EP_MASK = 2 };
 
+typedef uint32_t u2v __attribute__((ext_vector_type(2)));
+typedef uint32_t u4v __attribute__((ext_vector_type(4)));
+typedef float f2v __attribute__((ext_vector_type(2)));
+typedef __bf16 bf2v __attribute__((ext_vector_type(2)));
+typedef __bf16 bf8v __attribute__((ext_vector_type(8)));
+
+// bf16 roundings (to nearest even) of a and b, packed (a in the low half)
+__device__ __forceinline__ uint32_t bf16_pair(float a, float b) {
+    return __builtin_bit_cast(uint32_t, __builtin_convertvector(f2v{a, b}, bf2v));
+}
+
+// The three bf16 parts of a and of b, part i of both in word i (a in the low
+// half): part 0 rounds the value, part 1 what part 0 leaves, part 2 what parts
+// 0 and 1 leave; every difference is exact in fp32, and the last remainder has
+// at most eight significant bits, so the parts sum to the value exactly.
+__device__ __forceinline__ void split_pair(float a, float b, uint32_t (&w)[3]) {
+#pragma unroll
+    for (int i = 0; i < 3; ++i) {
+        w[i] = bf16_pair(a, b);
+        a -= __uint_as_float(w[i] << 16);
+        b -= __uint_as_float(w[i] & 0xFFFF0000u);
+    }
+}
+
+__device__ __forceinline__ f4 mfma_bf16(u4v a, u4v b, f4 c) {
+    return __builtin_amdgcn_mfma_f32_16x16x32_bf16(__builtin_bit_cast(bf8v, a),
+                                                   __builtin_bit_cast(bf8v, b), c, 0, 0, 0);
+}
+
 // Global -> register staging of one K chunk of a TM x TN output tile: each of
-// the 256 threads holds TM / 32 float4 of the a tile ([TM x 32]) and TN / 32 of
+// the 256 threads holds TM / 8 values of the a tile ([TM x 32]) and TN / 8 of
 // the b tile ([32 x TN]).
 template <int TM, int TN>
 struct Stage {
     float4 a[TM / 32], b[TN / 32];
 };
 
-// Sixteen zero bytes in device memory: a lane whose float4 lies outside its
+// Sixteen zero bytes in device memory: a lane whose value lies outside its
 // operand loads these instead. The choice is made on the address, before the
 // load, and the loaded registers are not touched again until they are written
 // to LDS. (A load under a lane condition compiles to a branch and an immediate
@@ -82,27 +127,29 @@ __device__ __attribute__((aligned(16))) float g_zero16[4] = {0.f, 0.f, 0.f, 0.f}
 __device__ __forceinline__ float4 ld4(bool ok, const float *p) {
     return *reinterpret_cast<const float4 *>(ok ? p : g_zero16);
 }
+__device__ __forceinline__ float ld1(bool ok, const float *p) { return *(ok ? p : g_zero16); }
 
+// ---- fp32 flavour: operands staged as fp32, v_mfma_f32_16x16x4f32 ----------
+//
 // LDS row stride of a k-major operand tile of width T ([k][x], floats): T + 16,
 // so that the four k rows an MFMA operand read touches per wave fall in four
 // different groups of 16 banks.
 __host__ __device__ constexpr int kmajor_stride(int T) { return T + 16; }
-// floats of one LDS operand tile of width T (k-major [32][T + 16] or
+// floats of one fp32 LDS operand tile of width T (k-major [32][T + 16] or
 // x-major [T][GMS])
-__host__ __device__ constexpr int tile_floats(int T) {
+__host__ __device__ constexpr int f32_tile_floats(int T) {
     return GK * kmajor_stride(T) > T * GMS ? GK * kmajor_stride(T) : T * GMS;
 }
 
-// One operand tile of width T (T = 32, 64 or 128; x is m for the a tile, n
-// for the b tile) and K chunk [k0, k0 + 32), thread t's float4 h (h < T / 32):
+// One operand tile of width T (T = 32 or 64; x is m for the a tile, n for the
+// b tile) and K chunk [k0, k0 + 32), thread t's float4 h (h < T / 32):
 //   loaded along x (k-major operand, P[k ld + x]):
 //     (k, x) = (t / (T/4) + (1024/T) h, 4 (t % (T/4)))
 //   loaded along k (x-major operand, P[x ld + k]):
 //     (x, k) = (t / (256/T), 4 (t % (256/T)) + (1024/T) h)
 template <bool KMAJOR, int T>
-__device__ __forceinline__ void fetch_operand(float4 (&r)[T / 32], const float *__restrict__ P,
-                                              int ld, int64_t xlim, int64_t x0, int64_t k0,
-                                              int64_t ke, int t) {
+__device__ __forceinline__ void fetch_f32(float4 (&r)[T / 32], const float *__restrict__ P, int ld,
+                                          int64_t xlim, int64_t x0, int64_t k0, int64_t ke, int t) {
 #pragma unroll
     for (int h = 0; h < T / 32; ++h) {
         if constexpr (KMAJOR) {
@@ -120,7 +167,7 @@ __device__ __forceinline__ void fetch_operand(float4 (&r)[T / 32], const float *
 // rows x 2 k columns an MFMA operand read touches per half wave land in 32
 // distinct banks), in 8-byte stores (the stride is not a multiple of 4).
 template <bool KMAJOR, int T>
-__device__ __forceinline__ void stash_operand(const float4 (&r)[T / 32], float *S, int t) {
+__device__ __forceinline__ void stash_f32(const float4 (&r)[T / 32], float *S, int t) {
 #pragma unroll
     for (int h = 0; h < T / 32; ++h) {
         if constexpr (KMAJOR) {
@@ -135,18 +182,100 @@ __device__ __forceinline__ void stash_operand(const float4 (&r)[T / 32], float *
     }
 }
 
-template <int OP, int TM, int TN>
+// ---- bf16x3 flavour: operands split into three bf16 parts, bf16 MFMA --------
+//
+// floats (4-byte words) of one split LDS operand tile of width T: three bf16
+// parts of [T][32], k inner
+__host__ __device__ constexpr int bf3_tile_floats(int T) { return 3 * T * GK / 2; }
+
+// Position in its row of element k of row x: the row's four 16-byte granules
+// are permuted by (x >> 2) & 3, so that 8 consecutive rows read at one granule,
+// and 16 rows written at one 8-byte half granule, fall in distinct banks.
+__device__ __forceinline__ int swz(int x, int k) { return (((k >> 3) ^ ((x >> 2) & 3)) << 3) | (k & 7); }
+
+// Thread t holds E = T / 8 values of one row x and k in [kr, kr + E):
+//   loaded along x (k-major operand, P[k ld + x]; a wave's lanes take
+//   consecutive x, so each of the E scalar loads is one contiguous row segment):
+//     x = t % T, kr = E (t / T)
+//   loaded along k (x-major operand, P[x ld + k]; E / 4 float4 loads):
+//     x = t / (32 / E), kr = E (t % (32 / E))
+template <bool KMAJOR, int T>
+__device__ __forceinline__ void fetch_bf3(float4 (&r)[T / 32], const float *__restrict__ P, int ld,
+                                          int64_t xlim, int64_t x0, int64_t k0, int64_t ke, int t) {
+    static_assert(T == 32 || T == 64, "operand tile width");
+    constexpr int E = T / 8;
+    if constexpr (KMAJOR) {
+        const int64_t x = x0 + t % T, k = k0 + E * (t / T);
+        float v[E];
+#pragma unroll
+        for (int j = 0; j < E; ++j) v[j] = ld1(x < xlim && k + j < ke, P + (k + j) * ld + x);
+#pragma unroll
+        for (int h = 0; h < T / 32; ++h) r[h] = make_float4(v[4 * h], v[4 * h + 1], v[4 * h + 2], v[4 * h + 3]);
+    } else {
+        const int64_t x = x0 + t / (32 / E), k = k0 + E * (t % (32 / E));
+#pragma unroll
+        for (int h = 0; h < T / 32; ++h) r[h] = ld4(x < xlim && k + 4 * h < ke, P + x * ld + k + 4 * h);
+    }
+}
+
+// Registers -> LDS: the thread's E values split into three bf16 parts, part p
+// written to row x of part tile p at swz(x, kr) in one 16-byte (E = 8) or
+// 8-byte (E = 4) store.
+template <bool KMAJOR, int T>
+__device__ __forceinline__ void stash_bf3(const float4 (&r)[T / 32], uint16_t *S, int t) {
+    constexpr int E = T / 8;
+    const int x = KMAJOR ? t % T : t / (32 / E), kr = KMAJOR ? E * (t / T) : E * (t % (32 / E));
+    uint32_t w[3][E / 2];
+#pragma unroll
+    for (int h = 0; h < T / 32; ++h) {
+        uint32_t q[3];
+        split_pair(r[h].x, r[h].y, q);
+#pragma unroll
+        for (int p = 0; p < 3; ++p) w[p][2 * h] = q[p];
+        split_pair(r[h].z, r[h].w, q);
+#pragma unroll
+        for (int p = 0; p < 3; ++p) w[p][2 * h + 1] = q[p];
+    }
+#pragma unroll
+    for (int p = 0; p < 3; ++p) {
+        uint16_t *d = S + (p * T + x) * GK + swz(x, kr);
+        if constexpr (E == 8)
+            *reinterpret_cast<u4v *>(d) = u4v{w[p][0], w[p][1], w[p][2], w[p][3]};
+        else
+            *reinterpret_cast<u2v *>(d) = u2v{w[p][0], w[p][1]};
+    }
+}
+
+// ---- the product ---------------------------------------------------------------
+
+// floats of one LDS operand tile of width T in either flavour
+__host__ __device__ constexpr int tile_floats(int T, bool bf3) {
+    return bf3 ? bf3_tile_floats(T) : f32_tile_floats(T);
+}
+
+template <int OP, int TM, int TN, bool BF3>
 __device__ __forceinline__ void gemm_fetch(Stage<TM, TN> &st, const float *__restrict__ A, int lda,
                                            const float *__restrict__ B, int ldb, int64_t M, int N,
                                            int64_t m0, int n0, int64_t k0, int64_t ke, int t) {
-    fetch_operand<OP == OP_TN, TM>(st.a, A, lda, M, m0, k0, ke, t);   // TN: a(m, k) = A[k lda + m]
-    fetch_operand<OP != OP_NT, TN>(st.b, B, ldb, N, n0, k0, ke, t);   // NT: b(k, n) = B[n ldb + k]
+    // TN: a(m, k) = A[k lda + m]; NT: b(k, n) = B[n ldb + k]
+    if constexpr (BF3) {
+        fetch_bf3<OP == OP_TN, TM>(st.a, A, lda, M, m0, k0, ke, t);
+        fetch_bf3<OP != OP_NT, TN>(st.b, B, ldb, N, n0, k0, ke, t);
+    } else {
+        fetch_f32<OP == OP_TN, TM>(st.a, A, lda, M, m0, k0, ke, t);
+        fetch_f32<OP != OP_NT, TN>(st.b, B, ldb, N, n0, k0, ke, t);
+    }
 }
 
-template <int OP, int TM, int TN>
+template <int OP, int TM, int TN, bool BF3>
 __device__ __forceinline__ void gemm_stash(const Stage<TM, TN> &st, float *As, float *Bs, int t) {
-    stash_operand<OP == OP_TN, TM>(st.a, As, t);
-    stash_operand<OP != OP_NT, TN>(st.b, Bs, t);
+    if constexpr (BF3) {
+        stash_bf3<OP == OP_TN, TM>(st.a, reinterpret_cast<uint16_t *>(As), t);
+        stash_bf3<OP != OP_NT, TN>(st.b, reinterpret_cast<uint16_t *>(Bs), t);
+    } else {
+        stash_f32<OP == OP_TN, TM>(st.a, As, t);
+        stash_f32<OP != OP_NT, TN>(st.b, Bs, t);
+    }
 }
 
 // C[m][n] = sum_k a(m, k) b(k, n) over k in [k_begin(z), k_end(z)), where
@@ -175,18 +304,18 @@ struct GemmArgs {
 };
 
 // LDS floats of one workgroup of a TM x TN product (two buffers of each operand)
-__host__ __device__ constexpr int gemm_lds_floats(int TM, int TN) {
-    return 2 * (tile_floats(TM) + tile_floats(TN));
+__host__ __device__ constexpr int gemm_lds_floats(int TM, int TN, bool bf3) {
+    return 2 * (tile_floats(TM, bf3) + tile_floats(TN, bf3));
 }
 
-// One output tile (bx, by) of split bz; lds holds gemm_lds_floats(TM, TN).
-template <int OP, int EP, int TM, int TN>
+// One output tile (bx, by) of split bz; lds holds gemm_lds_floats(TM, TN, BF3).
+template <int OP, int EP, int TM, int TN, bool BF3>
 __device__ __forceinline__ void gemm_block(const GemmArgs &g, int bx, int by, int bz,
                                            float *__restrict__ lds) {
     constexpr int MI = TM / 32, NJ = TN / 32;   // 16 x 16 MFMA tiles per wave
     constexpr int AS = kmajor_stride(TM), BS = kmajor_stride(TN);
-    float *As2[2] = {lds, lds + tile_floats(TM)};
-    float *Bs2[2] = {lds + 2 * tile_floats(TM), lds + 2 * tile_floats(TM) + tile_floats(TN)};
+    float *As2[2] = {lds, lds + tile_floats(TM, BF3)};
+    float *Bs2[2] = {lds + 2 * tile_floats(TM, BF3), lds + 2 * tile_floats(TM, BF3) + tile_floats(TN, BF3)};
     const float *__restrict__ A = g.A;
     const float *__restrict__ B = g.B;
     const float *__restrict__ G = g.G;
@@ -201,11 +330,13 @@ __device__ __forceinline__ void gemm_block(const GemmArgs &g, int bx, int by, in
     const int64_t kb = (int64_t)bz * kc;
     const int64_t ke = kb + kc < K ? kb + kc : K;
 
-    f4 acc[MI][NJ];
+    // acc: the products (fp32) or the leading part products a0 b0 (bf16x3);
+    // lo: the other five part products (bf16x3 only)
+    f4 acc[MI][NJ], lo[MI][NJ];
 #pragma unroll
     for (int i = 0; i < MI; ++i)
 #pragma unroll
-        for (int j = 0; j < NJ; ++j) acc[i][j] = f4{0.f, 0.f, 0.f, 0.f};
+        for (int j = 0; j < NJ; ++j) acc[i][j] = lo[i][j] = f4{0.f, 0.f, 0.f, 0.f};
 
     // NS chunks in flight: chunk c + NS is fetched into the registers chunk c
     // has just left, while chunk c is on the matrix cores. Chunks alternate
@@ -220,7 +351,7 @@ __device__ __forceinline__ void gemm_block(const GemmArgs &g, int bx, int by, in
     Stage<TM, TN> st[NS];
 #pragma unroll
     for (int q = 0; q < NS; ++q)
-        gemm_fetch<OP, TM, TN>(st[q], A, lda, B, ldb, M, N, m0, n0, kb + q * GK, ke, t);
+        gemm_fetch<OP, TM, TN, BF3>(st[q], A, lda, B, ldb, M, N, m0, n0, kb + q * GK, ke, t);
     // the mask of the epilogue, loaded now (clamped addresses, no lane condition)
     // so that its loads overlap the K loop instead of each waiting at the end
     float gm[EP == EP_MASK ? MI : 1][EP == EP_MASK ? NJ : 1][4];
@@ -238,28 +369,63 @@ __device__ __forceinline__ void gemm_block(const GemmArgs &g, int bx, int by, in
                 }
             }
     }
+    // fp32: eight k steps of 4 on the matrix cores.
+    // bf16x3: lane (li, lq) reads k in [8 lq, 8 lq + 8) of row li of each 16-row
+    // operand tile, for every part. The leading part product a0 b0 accumulates
+    // in acc, the five smaller ones (below 2^-7 |a b| together) in lo, smallest
+    // first, so that their roundings are relative to their own sum, not to the
+    // whole dot product; all tiles' product of one part pair go out back to
+    // back (independent accumulators).
     auto mfma_chunk = [&](int buf) __attribute__((always_inline)) {
-        const float *As = As2[buf], *Bs = Bs2[buf];
-        // eight k steps of 4 on the matrix cores
+        if constexpr (BF3) {
+            const uint16_t *As = reinterpret_cast<const uint16_t *>(As2[buf]);
+            const uint16_t *Bs = reinterpret_cast<const uint16_t *>(Bs2[buf]);
+            u4v a[MI][3], b[NJ][3];
 #pragma unroll
-        for (int ks = 0; ks < GK / 4; ++ks) {
-            const int kr = ks * 4 + lq;
-            float a[MI], b[NJ];
+            for (int p = 0; p < 3; ++p) {
 #pragma unroll
-            for (int i = 0; i < MI; ++i) {
-                const int m = wm * (TM / 2) + i * 16 + li;
-                a[i] = OP == OP_TN ? As[kr * AS + m] : As[m * GMS + kr];
+                for (int i = 0; i < MI; ++i)
+                    a[i][p] = *reinterpret_cast<const u4v *>(
+                        As + (p * TM + wm * (TM / 2) + i * 16 + li) * GK + swz(li, 8 * lq));
+#pragma unroll
+                for (int j = 0; j < NJ; ++j)
+                    b[j][p] = *reinterpret_cast<const u4v *>(
+                        Bs + (p * TN + wn * (TN / 2) + j * 16 + li) * GK + swz(li, 8 * lq));
             }
+            constexpr int PA[5] = {2, 1, 0, 1, 0}, PB[5] = {0, 1, 2, 0, 1};
 #pragma unroll
-            for (int j = 0; j < NJ; ++j) {
-                const int n = wn * (TN / 2) + j * 16 + li;
-                b[j] = OP == OP_NT ? Bs[n * GMS + kr] : Bs[kr * BS + n];
-            }
+            for (int q = 0; q < 5; ++q)
+#pragma unroll
+                for (int i = 0; i < MI; ++i)
+#pragma unroll
+                    for (int j = 0; j < NJ; ++j)
+                        lo[i][j] = mfma_bf16(a[i][PA[q]], b[j][PB[q]], lo[i][j]);
 #pragma unroll
             for (int i = 0; i < MI; ++i)
 #pragma unroll
-                for (int j = 0; j < NJ; ++j)
-                    acc[i][j] = __builtin_amdgcn_mfma_f32_16x16x4f32(a[i], b[j], acc[i][j], 0, 0, 0);
+                for (int j = 0; j < NJ; ++j) acc[i][j] = mfma_bf16(a[i][0], b[j][0], acc[i][j]);
+        } else {
+            const float *As = As2[buf], *Bs = Bs2[buf];
+#pragma unroll
+            for (int ks = 0; ks < GK / 4; ++ks) {
+                const int kr = ks * 4 + lq;
+                float a[MI], b[NJ];
+#pragma unroll
+                for (int i = 0; i < MI; ++i) {
+                    const int m = wm * (TM / 2) + i * 16 + li;
+                    a[i] = OP == OP_TN ? As[kr * AS + m] : As[m * GMS + kr];
+                }
+#pragma unroll
+                for (int j = 0; j < NJ; ++j) {
+                    const int n = wn * (TN / 2) + j * 16 + li;
+                    b[j] = OP == OP_NT ? Bs[n * GMS + kr] : Bs[kr * BS + n];
+                }
+#pragma unroll
+                for (int i = 0; i < MI; ++i)
+#pragma unroll
+                    for (int j = 0; j < NJ; ++j)
+                        acc[i][j] = __builtin_amdgcn_mfma_f32_16x16x4f32(a[i], b[j], acc[i][j], 0, 0, 0);
+            }
         }
     };
     int64_t c = 0;
@@ -267,9 +433,9 @@ __device__ __forceinline__ void gemm_block(const GemmArgs &g, int bx, int by, in
 #pragma unroll
         for (int q = 0; q < NS; ++q) {
             const int buf = (int)((c + q) & 1);
-            gemm_stash<OP, TM, TN>(st[q], As2[buf], Bs2[buf], t);
+            gemm_stash<OP, TM, TN, BF3>(st[q], As2[buf], Bs2[buf], t);
             __syncthreads();
-            gemm_fetch<OP, TM, TN>(st[q], A, lda, B, ldb, M, N, m0, n0, kb + (c + q + NS) * GK, ke, t);
+            gemm_fetch<OP, TM, TN, BF3>(st[q], A, lda, B, ldb, M, N, m0, n0, kb + (c + q + NS) * GK, ke, t);
             mfma_chunk(buf);
         }
     }
@@ -278,7 +444,7 @@ __device__ __forceinline__ void gemm_block(const GemmArgs &g, int bx, int by, in
     for (int q = 0; q < NS - 1; ++q) {
         if (c + q < nch) {
             const int buf = (int)((c + q) & 1);
-            gemm_stash<OP, TM, TN>(st[q], As2[buf], Bs2[buf], t);
+            gemm_stash<OP, TM, TN, BF3>(st[q], As2[buf], Bs2[buf], t);
             __syncthreads();
             mfma_chunk(buf);
         }
@@ -294,34 +460,36 @@ __device__ __forceinline__ void gemm_block(const GemmArgs &g, int bx, int by, in
             for (int v = 0; v < 4; ++v) {
                 const int64_t m = m0 + wm * (TM / 2) + i * 16 + 4 * lq + v;
                 if (m >= M || n >= N) continue;
-                float r = acc[i][j][v];
-                if constexpr (EP == EP_RELU) r = r > 0.0f ? r : 0.0f;           // eq. 12
+                float r = BF3 ? acc[i][j][v] + lo[i][j][v] : acc[i][j][v];
+                // eq. 12; a NaN passes (a diverged step must reach the loss: an
+                // infinite operand leaves NaN in its split parts)
+                if constexpr (EP == EP_RELU) r = r <= 0.0f ? 0.0f : r;
                 if constexpr (EP == EP_MASK) r = gm[i][j][v] > 0.0f ? r : 0.0f;    // eq. 17
                 Cz[m * ldc + n] = r;
             }
         }
 }
 
-template <int OP, int EP, int TM, int TN>
+template <int OP, int EP, int TM, int TN, bool BF3>
 __global__ __launch_bounds__(256) void k_gemm(const GemmArgs g) {
-    __shared__ __attribute__((aligned(16))) float lds[gemm_lds_floats(TM, TN)];
-    gemm_block<OP, EP, TM, TN>(g, blockIdx.x, blockIdx.y, blockIdx.z, lds);
+    __shared__ __attribute__((aligned(16))) float lds[gemm_lds_floats(TM, TN, BF3)];
+    gemm_block<OP, EP, TM, TN, BF3>(g, blockIdx.x, blockIdx.y, blockIdx.z, lds);
 }
 
 // Two independent products in one launch (a one-dimensional grid): blocks
 // [0, g1.gx g1.gy g1.gz) compute the first, the rest the second. With both
 // resident together the CUs hold twice the workgroups of either alone.
-template <int OP1, int EP1, int TM1, int TN1, int OP2, int EP2, int TM2, int TN2>
+template <int OP1, int EP1, int TM1, int TN1, int OP2, int EP2, int TM2, int TN2, bool BF3>
 __global__ __launch_bounds__(256) void k_gemm_pair(const GemmArgs g1, const GemmArgs g2) {
-    constexpr int L1 = gemm_lds_floats(TM1, TN1), L2 = gemm_lds_floats(TM2, TN2);
+    constexpr int L1 = gemm_lds_floats(TM1, TN1, BF3), L2 = gemm_lds_floats(TM2, TN2, BF3);
     __shared__ __attribute__((aligned(16))) float lds[L1 > L2 ? L1 : L2];
     const int n1 = g1.gx * g1.gy * g1.gz;
     int b = blockIdx.x;
     if (b < n1) {
-        gemm_block<OP1, EP1, TM1, TN1>(g1, b % g1.gx, (b / g1.gx) % g1.gy, b / (g1.gx * g1.gy), lds);
+        gemm_block<OP1, EP1, TM1, TN1, BF3>(g1, b % g1.gx, (b / g1.gx) % g1.gy, b / (g1.gx * g1.gy), lds);
     } else {
         b -= n1;
-        gemm_block<OP2, EP2, TM2, TN2>(g2, b % g2.gx, (b / g2.gx) % g2.gy, b / (g2.gx * g2.gy), lds);
+        gemm_block<OP2, EP2, TM2, TN2, BF3>(g2, b % g2.gx, (b / g2.gx) % g2.gy, b / (g2.gx * g2.gy), lds);
     }
 }
 
@@ -631,7 +799,10 @@ static size_t deep_ws_floats(int h, int L, int64_t mb) {
 // gradient of W_1); a single product (not a pair) narrows that to 32 x 32 where
 // it would still leave fewer than four. Larger tiles (128 x 64, 128 x 128) halve the operand
 // traffic per MFMA but leave one or two workgroups per CU on the 1024-wide
-// products, which measured 6-8 % slower than four.
+// products, which measured 6-8 % slower than four. The 64 x 64 tiles (the
+// MFMA-heavy products of wide layers) run the bf16x3 flavour, the narrower
+// ones (latency-bound, few chunks each) the fp32 one: bf16x3 made the 1024-wide
+// net 8 % faster and the 256-wide ones 3-6 % slower.
 static GemmArgs gemm_args(const float *A, int lda, const float *B, int ldb, float *C, int ldc,
                           int64_t c_split, int64_t M, int N, int64_t K, int splits, int64_t kc,
                           const float *G, int ldg, bool *small) {
@@ -670,12 +841,12 @@ static hipError_t gemm(hipStream_t st, const float *A, int lda, const float *B, 
         // workgroups per CU
         GemmArgs gn = g;
         gn.gy = (N + 31) / 32;
-        hipLaunchKernelGGL((k_gemm<OP, EP, 32, 32>), dim3((unsigned)gn.gx, (unsigned)gn.gy, (unsigned)gn.gz),
+        hipLaunchKernelGGL((k_gemm<OP, EP, 32, 32, false>), dim3((unsigned)gn.gx, (unsigned)gn.gy, (unsigned)gn.gz),
                            dim3(256), 0, st, gn);
     } else if (small)
-        hipLaunchKernelGGL((k_gemm<OP, EP, 32, GT>), grid, dim3(256), 0, st, g);
+        hipLaunchKernelGGL((k_gemm<OP, EP, 32, GT, false>), grid, dim3(256), 0, st, g);
     else
-        hipLaunchKernelGGL((k_gemm<OP, EP, GT, GT>), grid, dim3(256), 0, st, g);
+        hipLaunchKernelGGL((k_gemm<OP, EP, GT, GT, true>), grid, dim3(256), 0, st, g);
     return hipGetLastError();
 }
 
@@ -685,13 +856,13 @@ static hipError_t gemm_pair(hipStream_t st, const GemmArgs &g1, bool small1, con
                             bool small2) {
     const dim3 grid((unsigned)(g1.gx * g1.gy * g1.gz + g2.gx * g2.gy * g2.gz));
     if (small1 && small2)
-        hipLaunchKernelGGL((k_gemm_pair<OP1, EP1, 32, GT, OP2, EP2, 32, GT>), grid, dim3(256), 0, st, g1, g2);
+        hipLaunchKernelGGL((k_gemm_pair<OP1, EP1, 32, GT, OP2, EP2, 32, GT, false>), grid, dim3(256), 0, st, g1, g2);
     else if (small1)
-        hipLaunchKernelGGL((k_gemm_pair<OP1, EP1, 32, GT, OP2, EP2, GT, GT>), grid, dim3(256), 0, st, g1, g2);
+        hipLaunchKernelGGL((k_gemm_pair<OP1, EP1, 32, GT, OP2, EP2, GT, GT, false>), grid, dim3(256), 0, st, g1, g2);
     else if (small2)
-        hipLaunchKernelGGL((k_gemm_pair<OP1, EP1, GT, GT, OP2, EP2, 32, GT>), grid, dim3(256), 0, st, g1, g2);
+        hipLaunchKernelGGL((k_gemm_pair<OP1, EP1, GT, GT, OP2, EP2, 32, GT, false>), grid, dim3(256), 0, st, g1, g2);
     else
-        hipLaunchKernelGGL((k_gemm_pair<OP1, EP1, GT, GT, OP2, EP2, GT, GT>), grid, dim3(256), 0, st, g1, g2);
+        hipLaunchKernelGGL((k_gemm_pair<OP1, EP1, GT, GT, OP2, EP2, GT, GT, true>), grid, dim3(256), 0, st, g1, g2);
     return hipGetLastError();
 }
 

@@ -58,13 +58,20 @@ def _gauss_net(rng, h, L):
 
 def _kink_free(X, P, h, L, idx):
     """The rows of idx whose pre-activations all lie farther from zero than a
-    bound on the device's fp32 error. Layer l computes Z = H_{l-1} W_l, a sum of
-    K products, from an input each entry of which is within e_{l-1} of exact
-    (e_0 = 0: X is exact); the device's Z is then within
-    e_l = (K + 2) u sum_k (|H_k| + e_k) |W_kj| + sum_k e_k |W_kj| of exact (the
-    fp32 sum of K terms, each off by at most e_k |W_kj|; ReLU is 1-Lipschitz, so
-    e_l also bounds the layer's output). Where |Z| > e_l the device's ReLU mask
-    equals the exact one."""
+    bound on the device's error. Layer l computes Z = H_{l-1} W_l, a sum of K
+    products, from an input each entry of which is within e_{l-1} of exact
+    (e_0 = 0: X is exact). The device forms each product a b from three-part
+    bf16 splits of a and b (a = a0 + a1 + a2 exactly, |a1| <= 2^-8 (1 + 2^-8)|a|,
+    |a2| <= 2^-16 |a|): a0 b0 summed over k in fp32 (K terms, within
+    (1 + 2^-8)^2 |a b| each: at most 1.016 K u sum |a b| of rounding), the five
+    part products with i + j in {1, 2} in a second fp32 sum (5 K terms, below
+    1.02 * 2^-7 |a b| per k together: at most 0.04 K u), one addition of the
+    two (1.02 u) and the three dropped part products (at most 2.01 u |a b|).
+    So the device's Z is within
+    e_l = (1.1 K + 4) u sum_k (|H_k| + e_k) |W_kj| + sum_k e_k |W_kj| of exact
+    (each term is also off by at most e_k |W_kj| through its input; ReLU is
+    1-Lipschitz, so e_l also bounds the layer's output). Where |Z| > e_l the
+    device's ReLU mask equals the exact one."""
     Ws, _ = oracle.deep_split(np.asarray(P, np.float64), D, h, L)
     Hp = np.asarray(X, np.float64)[idx]
     Ep = np.zeros_like(Hp)
@@ -74,7 +81,7 @@ def _kink_free(X, P, h, L, idx):
         A = np.abs(W)
         Z = Hp @ W
         prop = Ep @ A
-        E = (K + 2) * U32 * (np.abs(Hp) @ A + prop) + prop
+        E = (1.1 * K + 4) * U32 * (np.abs(Hp) @ A + prop) + prop
         ok &= np.all(np.abs(Z) > E, axis=1)
         Hp, Ep = np.maximum(Z, 0.0), E
     return np.ascontiguousarray(idx[ok])
@@ -111,6 +118,21 @@ def test_forward_dyadic_is_exact(mlp, h, L):
     rng = np.random.default_rng(10 * h + L)
     X, Y, P = _dyadic(rng, 1000, h, L)
     ctx, _ = _ctx(mlp, P, h, L, 256)             # 1000 rows: four chunks of max_batch
+    got = mlp.mlp_deep_forward(ctx, _to(X)).cpu().numpy()
+    ref = oracle.deep_forward(X, P, D, h, L)
+    assert np.array_equal(got, ref.astype(np.float32))
+    mlp.mlp_deep_check_errors(ctx)
+
+
+def test_forward_dyadic_is_exact_wide_tiles(mlp):
+    """h = 1024 at 2100 rows: the forward products run 64 x 64 tiles, the bf16x3
+    flavour (three-part bf16 splits on the bf16 matrix cores); on dyadic inputs
+    every part product and partial sum is exact, so the output must match the
+    oracle bitwise, as in the fp32 flavour."""
+    h, L = 1024, 2
+    rng = np.random.default_rng(1024)
+    X, Y, P = _dyadic(rng, 2100, h, L)
+    ctx, _ = _ctx(mlp, P, h, L, 2100)
     got = mlp.mlp_deep_forward(ctx, _to(X)).cpu().numpy()
     ref = oracle.deep_forward(X, P, D, h, L)
     assert np.array_equal(got, ref.astype(np.float32))
@@ -167,6 +189,29 @@ def test_gradients_gaussian(mlp, h, L, B):
     ref, _, _ = oracle.deep_grad(d.X, d.Y, P, D, h, L, idx=rows)
     e = rel(dP.cpu().numpy(), ref)
     print("kink-free batch of %d rows: gradient rel %.3e" % (B, e))
+    assert e <= 1e-5
+    mlp.mlp_deep_check_errors(ctx)
+
+
+def test_gradients_gaussian_wide_tiles(mlp):
+    """h = 1024 with a batch of 2100 kink-free rows: every product of the step
+    that runs 64 x 64 tiles (the forward, the W_2 gradient paired with the
+    back-propagation) takes the bf16x3 flavour; gradients and loss at 1e-5 as
+    in the fp32-flavour cases (one oracle pass: 2100 rows at h = 1024 take the
+    fp64 oracle about 16 s)."""
+    h, L, B = 1024, 2, 2100
+    rng = np.random.default_rng(4096)
+    d = datagen.make_data(5000, 32, seed=6, with_perm=False)
+    P = _gauss_net(rng, h, L)
+    ctx, _ = _ctx(mlp, P, h, L, B)
+    cand = rng.integers(0, 5000, size=8 * B).astype(np.int32)
+    rows = _kink_free(d.X, P, h, L, cand)[:B]
+    assert len(rows) == B, (len(rows), B)
+    dP, loss = mlp.mlp_deep_backward(ctx, _to(d.X), _to(d.Y), _to(rows))
+    ref, rL, _ = oracle.deep_grad(d.X, d.Y, P, D, h, L, idx=rows)
+    assert abs(float(loss.cpu()[0]) - rL) <= 1e-5 * rL
+    e = rel(dP.cpu().numpy(), ref)
+    print("kink-free batch of %d rows at h = 1024: gradient rel %.3e" % (B, e))
     assert e <= 1e-5
     mlp.mlp_deep_check_errors(ctx)
 
