@@ -59,6 +59,7 @@
 #include <stdint.h>
 #include <string.h>
 
+#include "bf16x3.h"
 #include "lanes.h"
 #include "mlp.h"
 #include "mlp_internal.h"
@@ -76,35 +77,6 @@ constexpr int DEEP_MAX_LAYERS = 8;
 
 enum { OP_NN = 0, OP_TN = 1, OP_NT = 2 };
 enum { EP_NONE = 0, EP_RELU = 1, EP_MASK = 2 };
-
-typedef uint32_t u2v __attribute__((ext_vector_type(2)));
-typedef uint32_t u4v __attribute__((ext_vector_type(4)));
-typedef float f2v __attribute__((ext_vector_type(2)));
-typedef __bf16 bf2v __attribute__((ext_vector_type(2)));
-typedef __bf16 bf8v __attribute__((ext_vector_type(8)));
-
-// bf16 roundings (to nearest even) of a and b, packed (a in the low half)
-__device__ __forceinline__ uint32_t bf16_pair(float a, float b) {
-    return __builtin_bit_cast(uint32_t, __builtin_convertvector(f2v{a, b}, bf2v));
-}
-
-// The three bf16 parts of a and of b, part i of both in word i (a in the low
-// half): part 0 rounds the value, part 1 what part 0 leaves, part 2 what parts
-// 0 and 1 leave; every difference is exact in fp32, and the last remainder has
-// at most eight significant bits, so the parts sum to the value exactly.
-__device__ __forceinline__ void split_pair(float a, float b, uint32_t (&w)[3]) {
-#pragma unroll
-    for (int i = 0; i < 3; ++i) {
-        w[i] = bf16_pair(a, b);
-        a -= __uint_as_float(w[i] << 16);
-        b -= __uint_as_float(w[i] & 0xFFFF0000u);
-    }
-}
-
-__device__ __forceinline__ f4 mfma_bf16(u4v a, u4v b, f4 c) {
-    return __builtin_amdgcn_mfma_f32_16x16x32_bf16(__builtin_bit_cast(bf8v, a),
-                                                   __builtin_bit_cast(bf8v, b), c, 0, 0, 0);
-}
 
 // Global -> register staging of one K chunk of a TM x TN output tile: each of
 // the 256 threads holds TM / 8 values of the a tile ([TM x 32]) and TN / 8 of

@@ -1,26 +1,34 @@
-// forward.hip -- the forward pass over many rows (eqs. 11-13) on fp32 MFMA,
-// for inference and full-dataset evaluation (mlp_forward).
+// forward.hip -- the forward pass over many rows (eqs. 11-13), for inference
+// and full-dataset evaluation (mlp_forward), with fp32 products formed on the
+// bf16 matrix cores.
 //
 // Per sample the pass is 2 * 32 * h FLOP of the layer-1 contraction plus 2 h
 // of the output product against 132 bytes of HBM traffic (an X row and its
-// output; 4 more with a row index): at ~128 FLOP/byte for h = 256 it is a dense
-// contraction bound by the matrix cores, not by HBM.
+// output; 4 more with a row index).
 //
-// A wave keeps the weights of up to 256 hidden units in registers for its whole
-// life, as the B operands of v_mfma_f32_16x16x4f32 (16 unit tiles x 8 k steps)
-// plus one W2 value per unit tile, and streams 16-row tiles of X:
+// The 32-deep contraction of a 16-row tile with a 16-unit tile is one
+// v_mfma_f32_16x16x32_bf16 per part product: X and W1 are split into three
+// bf16 parts each (bf16x3.h) and the six part products with i + j <= 2 are
+// accumulated in fp32, smallest first -- six 16-cycle MFMAs where fp32 MFMA
+// takes eight of 32 cycles, and a bf16 MFMA does not hold up the other waves
+// of its SIMD.
+//
+// A wave keeps the split weights of up to 128 hidden units in registers for its
+// whole life (three parts of W1[8 lq .. 8 lq + 7][unit] per unit tile, 12
+// VGPRs, plus one W2 value) and streams 16-row tiles of X:
 //   lane (li, lq) = (lane % 16, lane / 16) loads X[row li][8 lq .. 8 lq + 7]
-//   (two 16-byte loads) and feeds k = 8 lq + t to MFMA step t, so eight MFMAs
-//   accumulate Z1[4 lq + v][unit 16 u + li] of unit tile u in acc[u][v];
+//   (two 16-byte loads), which is its A operand of the MFMA, and splits it; the
+//   MFMAs accumulate Z1[4 lq + v][unit 16 u + li] of unit tile u in acc[u][v];
 //   ReLU and the W2 product stay in registers (eqs. 12-13), and a DPP
 //   butterfly sums each row's 16 unit lanes.
-// For h > 256 the waves of a workgroup split the units of one row tile and add
+// For h > 128 the waves of a workgroup split the units of one row tile and add
 // their partial outputs in LDS in a fixed order. The next tile's rows are
 // loaded while the current tile is on the matrix cores.
 #include <hip/hip_runtime.h>
 
 #include <stdint.h>
 
+#include "bf16x3.h"
 #include "lanes.h"
 #include "mlp.h"
 #include "mlp_internal.h"
@@ -29,18 +37,20 @@ namespace mlp {
 
 template <int H>
 struct FwdShape {
-    static constexpr int UW = H < 256 ? H : 256;   // units per wave
+    static constexpr int UW = H < 128 ? H : 128;   // units per wave
     static constexpr int NUT = UW / 16;            // unit tiles per wave
-    static constexpr int WPT = H / UW;             // waves per row tile: 1, 2 or 4
-    static constexpr int TPI = 4 / WPT;            // row tiles per workgroup iteration
-    // workgroups per CU the register budget allows (a wave holds 8.5 UW weight
-    // registers plus 4 NUT accumulators): small nets need more waves in flight
-    // to keep enough row loads outstanding
-    static constexpr int WG_PER_CU = UW <= 32 ? 8 : UW <= 64 ? 4 : UW <= 128 ? 3 : 2;
-    static_assert(H % 16 == 0 && WPT * UW == H && (WPT == 1 || WPT == 2 || WPT == 4), "shape");
+    static constexpr int WPT = H / UW;             // waves per row tile: 1, 2, 4 or 8
+    static constexpr int WAVES = WPT > 4 ? WPT : 4;   // waves per workgroup
+    static constexpr int TPI = WAVES / WPT;        // row-tile slots per workgroup iteration
+    // row tiles per slot and iteration: the HBM-bound h = 32 keeps two tiles of
+    // loads in flight per wave
+    static constexpr int RT = H == 32 ? 2 : 1;
+    // waves per SIMD the register budget allows (a wave holds 13 registers per
+    // unit tile of weights and 4 of accumulators, and about 40 more): small
+    // nets need more waves in flight to keep enough row loads outstanding
+    static constexpr int WAVES_PER_SIMD = NUT <= 2 ? 6 : NUT <= 4 ? 4 : WPT == 1 ? 3 : 2;
+    static_assert(H % 16 == 0 && WPT * UW == H && WPT <= 8, "shape");
 };
-
-constexpr int FWD_THREADS = 256;
 
 // Rows of one 16-row tile as MFMA A operands: lane (li, lq) holds
 // X[r_t][8 lq .. 8 lq + 7] of batch position t = r0 + li (zeros past B).
@@ -76,55 +86,57 @@ __device__ __forceinline__ RowTile load_rows(const float *__restrict__ X, int64_
 }
 
 template <int H>
-__global__ __launch_bounds__(FWD_THREADS, FwdShape<H>::WG_PER_CU) void k_forward(
+__global__ __launch_bounds__(64 * FwdShape<H>::WAVES, FwdShape<H>::WAVES_PER_SIMD) void k_forward(
     const float *__restrict__ X, int64_t n_rows, const int32_t *__restrict__ idx, int64_t B,
     const float *__restrict__ W1, const float *__restrict__ W2, float *__restrict__ ypred,
     int32_t *err) {
     using S = FwdShape<H>;
-    constexpr int NUT = S::NUT, WPT = S::WPT, TPI = S::TPI;
-    __shared__ float part[4][16];   // partial outputs of the waves of a row tile (WPT > 1)
+    constexpr int NUT = S::NUT, WPT = S::WPT, TPI = S::TPI, RT = S::RT;
+    __shared__ float part[S::WAVES][16];   // partial outputs of the waves of a row tile (WPT > 1)
 
     const int lane = threadIdx.x & 63;
     const int wave = __builtin_amdgcn_readfirstlane(threadIdx.x >> 6);
     const int li = lane & 15, lq = lane >> 4;
     const int wt = wave / WPT;   // row-tile slot within an iteration
-    const int wu = wave % WPT;   // unit block: units [wu * 256, wu * 256 + 256)
+    const int wu = wave % WPT;   // unit block: units [wu * UW, wu * UW + UW)
 
-    // the wave's weights, for its whole life: W1[8 lq + t][unit], W2[unit]
-    float w1b[NUT][8], w2v[NUT];
+    // the wave's weights, for its whole life: the parts of W1[8 lq + t][unit]
+    // (t = 0..7), and W2[unit]
+    u4v w1p[NUT][3];
+    float w2v[NUT];
 #pragma unroll
     for (int u = 0; u < NUT; ++u) {
         const int unit = wu * S::UW + 16 * u + li;
+        uint32_t w[4][3];
 #pragma unroll
-        for (int t = 0; t < 8; ++t) w1b[u][t] = W1[(8 * lq + t) * H + unit];
+        for (int t = 0; t < 4; ++t)
+            split_pair(W1[(8 * lq + 2 * t) * H + unit], W1[(8 * lq + 2 * t + 1) * H + unit], w[t]);
+#pragma unroll
+        for (int p = 0; p < 3; ++p) w1p[u][p] = u4v{w[0][p], w[1][p], w[2][p], w[3][p]};
         w2v[u] = W2[unit];
     }
 
-    const int64_t ntiles = (B + 15) / 16;
-    const int64_t iters = (ntiles + TPI - 1) / TPI;
-    int64_t it = blockIdx.x;
-    const int64_t r0f = (it * TPI + wt) * 16;
-    RowTile cur = load_rows(X, n_rows, idx, B, r0f, load_index(idx, B, r0f + li), li, lq, err);
-    int32_t ixn = load_index(idx, B, ((it + gridDim.x) * TPI + wt) * 16 + li);
-    __builtin_amdgcn_s_waitcnt(0x0F70);   // vmcnt(0)
-    for (; it < iters; it += gridDim.x) {
-        const int64_t r0 = (it * TPI + wt) * 16;
-        // the next iteration's rows, in flight while this tile is computed, and
-        // the index of the iteration after it
-        const int64_t r0n = ((it + gridDim.x) * TPI + wt) * 16;
-        const RowTile nxt = load_rows(X, n_rows, idx, B, r0n, ixn, li, lq, err);
-        ixn = load_index(idx, B, ((it + 2 * (int64_t)gridDim.x) * TPI + wt) * 16 + li);
-
-        // eq. 11: Z1 tile = X tile W1 (8 k steps of 4 per unit tile)
+    // one 16-row tile rt at batch row r0: eq. 11 (the six part products
+    // smallest first, every unit tile's product of one part pair back to back),
+    // ReLU and the W2 product in registers (eqs. 12-13), the row sums out
+    auto tile = [&](const RowTile &rt, int64_t r0) __attribute__((always_inline)) {
+        u4v xp[3];
+        {
+            uint32_t w[4][3];
+#pragma unroll
+            for (int t = 0; t < 4; ++t) split_pair(rt.x[2 * t], rt.x[2 * t + 1], w[t]);
+#pragma unroll
+            for (int p = 0; p < 3; ++p) xp[p] = u4v{w[0][p], w[1][p], w[2][p], w[3][p]};
+        }
+        constexpr int PA[6] = {2, 1, 0, 1, 0, 0}, PB[6] = {0, 1, 2, 0, 1, 0};
         f4 acc[NUT];
 #pragma unroll
         for (int u = 0; u < NUT; ++u) acc[u] = f4{0.f, 0.f, 0.f, 0.f};
 #pragma unroll
-        for (int t = 0; t < 8; ++t)
+        for (int q = 0; q < 6; ++q)
 #pragma unroll
-            for (int u = 0; u < NUT; ++u)
-                acc[u] = __builtin_amdgcn_mfma_f32_16x16x4f32(cur.x[t], w1b[u][t], acc[u], 0, 0, 0);
-        // eqs. 12-13: the lane's share of Ypred for rows 4 lq + v, units ascending
+            for (int u = 0; u < NUT; ++u) acc[u] = mfma_bf16(xp[PA[q]], w1p[u][PB[q]], acc[u]);
+        // the lane's share of Ypred for rows 4 lq + v, units ascending
         float yp[4] = {0.f, 0.f, 0.f, 0.f};
 #pragma unroll
         for (int u = 0; u < NUT; ++u)
@@ -149,7 +161,34 @@ __global__ __launch_bounds__(FWD_THREADS, FwdShape<H>::WG_PER_CU) void k_forward
             }
             __syncthreads();
         }
-        cur = nxt;
+    };
+
+    // iteration it: tiles (it TPI + wt) RT + j, j < RT, of this wave
+    const int64_t ntiles = (B + 15) / 16;
+    const int64_t iters = (ntiles + TPI * RT - 1) / (TPI * RT);
+    auto row0 = [&](int64_t i, int j) { return ((i * TPI + wt) * RT + j) * 16; };
+    int64_t it = blockIdx.x;
+    RowTile cur[RT];
+    int32_t ixn[RT];
+#pragma unroll
+    for (int j = 0; j < RT; ++j) {
+        cur[j] = load_rows(X, n_rows, idx, B, row0(it, j), load_index(idx, B, row0(it, j) + li), li, lq, err);
+        ixn[j] = load_index(idx, B, row0(it + gridDim.x, j) + li);
+    }
+    __builtin_amdgcn_s_waitcnt(0x0F70);   // vmcnt(0)
+    for (; it < iters; it += gridDim.x) {
+        // the next iteration's rows, in flight while these tiles are computed,
+        // and the indices of the iteration after it
+        RowTile nxt[RT];
+#pragma unroll
+        for (int j = 0; j < RT; ++j) {
+            nxt[j] = load_rows(X, n_rows, idx, B, row0(it + gridDim.x, j), ixn[j], li, lq, err);
+            ixn[j] = load_index(idx, B, row0(it + 2 * (int64_t)gridDim.x, j) + li);
+        }
+#pragma unroll
+        for (int j = 0; j < RT; ++j) tile(cur[j], row0(it, j));
+#pragma unroll
+        for (int j = 0; j < RT; ++j) cur[j] = nxt[j];
     }
 }
 
@@ -158,10 +197,11 @@ static hipError_t launch_forward_h(const Ctx &c, const float *X, int64_t n_rows,
                                    const int32_t *idx, int64_t B, float *ypred) {
     using S = FwdShape<H>;
     const int64_t ntiles = (B + 15) / 16;
-    const int64_t iters = (ntiles + S::TPI - 1) / S::TPI;
-    const int64_t cap = S::WG_PER_CU * (int64_t)(c.num_cu > 0 ? c.num_cu : 256);
+    const int64_t iters = (ntiles + S::TPI * S::RT - 1) / (S::TPI * S::RT);
+    // resident workgroups: WAVES_PER_SIMD waves on each of a CU's four SIMDs
+    const int64_t cap = (int64_t)S::WAVES_PER_SIMD * 4 / S::WAVES * (c.num_cu > 0 ? c.num_cu : 256);
     const int grid = (int)(iters < cap ? iters : cap);
-    hipLaunchKernelGGL((k_forward<H>), dim3(grid), dim3(FWD_THREADS), 0, c.stream, X, n_rows, idx,
+    hipLaunchKernelGGL((k_forward<H>), dim3(grid), dim3(64 * S::WAVES), 0, c.stream, X, n_rows, idx,
                        B, c.W1, c.W2, ypred, &c.ctl->err);
     return hipGetLastError();
 }
