@@ -107,6 +107,25 @@ def test_forward_full_dataset_sampled(mlp, k):
     assert rel(got, ref) < 1e-5
 
 
+@pytest.mark.parametrize("h", [32, 64])
+def test_forward_full_dataset_sampled_narrow(mlp, h):
+    """The narrow nets over all 10M rows of the largest workload's X in the
+    forward benchmark's launch shape (at h = 32 two row tiles per wave per
+    iteration): 20,000 sampled outputs against the oracle, every output finite."""
+    w, d = _workload_data(4)
+    net = datagen.make_data(1, h, seed=2000 + h, with_perm=False)
+    ctx, _, _ = _ctx(mlp, net.W1, net.W2, 64)
+    out = mlp.mlp_forward(ctx, _to(d.X))
+    torch.cuda.synchronize()
+    mlp.mlp_check_errors(ctx)
+    assert bool(torch.isfinite(out).all())
+    sample = np.random.default_rng(h).integers(0, w.n, size=20000).astype(np.int64)
+    sample[:2] = [0, w.n - 1]
+    got = out.cpu().numpy()[sample]
+    ref = oracle.forward(d.X, net.W1, net.W2, idx=sample.astype(np.int32))
+    assert rel(got, ref) < 1e-5
+
+
 # --- per-step gradients ----------------------------------------------------------
 
 def _check_grad(mlp, h, B, n=5000, seed=0, idx_none=False, strategy=None):
