@@ -16,7 +16,9 @@
 //   k_gemm<NN, RELU>   the forward of a layer, ReLU in the epilogue
 //   k_gemm<TN, NONE>   dW_l = H_{l-1}^T G_l, split over row chunks (grid z);
 //                      each chunk writes its own partial, summed in chunk order
-//   k_gemm<NT, MASK>   G_{l-1} = (G_l W_l^T) masked by H_{l-1} > 0
+//   k_gemm<NT, MASK>   G_{l-1} = (G_l W_l^T) masked by H_{l-1} > 0; into
+//                      layer 1 its epilogue also forms each row tile's
+//                      partial of dW_1 = X^T G_1 (no launch of its own)
 //   k_gemm_pair        the weight gradient and the back-propagation of one
 //                      layer (both read G_l, neither reads the other's output)
 //                      in one launch
@@ -76,7 +78,10 @@ constexpr int OUT_CHUNKS_MAX = 256;   // row chunks of the output layer (dw_o pa
 constexpr int DEEP_MAX_LAYERS = 8;
 
 enum { OP_NN = 0, OP_TN = 1, OP_NT = 2 };
-enum { EP_NONE = 0, EP_RELU = 1, EP_MASK = 2 };
+// Epilogues: none; ReLU (eq. 12); the ReLU mask of eq. 17; the mask and, from
+// the masked tile, the tile's share of dW_1 = X^T G_1 (eq. 18 for the first
+// layer, see gemm_block)
+enum { EP_NONE = 0, EP_RELU = 1, EP_MASK = 2, EP_MASK_DW1 = 3 };
 
 // Global -> register staging of one K chunk of a TM x TN output tile: each of
 // the 256 threads holds TM / 8 values of the a tile ([TM x 32]) and TN / 8 of
@@ -270,14 +275,72 @@ struct GemmArgs {
     int64_t c_split, M;
     int N;
     int64_t K, kc;
-    const float *G;   // mask operand of the MASK epilogue
+    const float *G;   // mask operand of the MASK epilogues
     int ldg;
     int gx, gy, gz;   // grid of this product, in tiles
+    // MASK_DW1: the layer's input rows X [M x D_IN] and where row tile bx
+    // writes its partial of dW_1 ([D_IN x N] at dw1 + bx * dw1_split)
+    const float *X;
+    float *dw1;
+    int64_t dw1_split;
 };
 
 // LDS floats of one workgroup of a TM x TN product (two buffers of each operand)
 __host__ __device__ constexpr int gemm_lds_floats(int TM, int TN, bool bf3) {
     return 2 * (tile_floats(TM, bf3) + tile_floats(TN, bf3));
+}
+
+// The MASK_DW1 epilogue's second half: the workgroup's tile of G_1 (rows
+// [m0, m0 + TM) of the batch, units [n0, n0 + TN); masked, in g, rows past M
+// zero) times the same rows of X gives that row tile's partial of
+// dW_1 = X^T G_1 (eq. 18 at the first layer) for those units, a sum over the
+// tile's TM rows in a fixed order. Both operands go through LDS (the K loop is
+// done with it); the product is TM / 4 steps of v_mfma_f32_16x16x4f32 per 16 x 16
+// output tile, two output tiles per wave (D_IN = 32 inputs x TN = 64 units).
+template <int TM, int TN, int MI, int NJ>
+__device__ __forceinline__ void dw1_partial(const GemmArgs &g, int bx, int by, const f4 (&gt)[MI][NJ],
+                                            float *__restrict__ lds) {
+    static_assert(TN == 64 && D_IN == 32, "dW_1 partial tile");
+    constexpr int XS = D_IN + 1, GS = TN + 1;   // LDS row strides (floats)
+    float *Xs = lds, *Gs = lds + TM * XS;
+    const int t = threadIdx.x;
+    const int lane = t & 63, wave = t >> 6;
+    const int li = lane & 15, lq = lane >> 4;
+    const int wm = wave >> 1, wn = wave & 1;
+    const int64_t m0 = (int64_t)bx * TM;
+    __syncthreads();   // every wave is done with the K loop's LDS
+#pragma unroll
+    for (int e = t; e < TM * D_IN; e += 256) {
+        const int r = e / D_IN, k = e % D_IN;
+        const int64_t m = m0 + r;
+        Xs[r * XS + k] = m < g.M ? g.X[m * D_IN + k] : 0.0f;
+    }
+#pragma unroll
+    for (int i = 0; i < MI; ++i)
+#pragma unroll
+        for (int j = 0; j < NJ; ++j)
+#pragma unroll
+            for (int v = 0; v < 4; ++v)
+                Gs[(wm * (TM / 2) + i * 16 + 4 * lq + v) * GS + wn * (TN / 2) + j * 16 + li] = gt[i][j][v];
+    __syncthreads();
+    // wave w: inputs 16 (w & 1) .. + 15, units 32 (w >> 1) .. + 31 (two tiles)
+    const int it = wave & 1, ub = (wave >> 1) * 32;
+    f4 p[2] = {f4{0.f, 0.f, 0.f, 0.f}, f4{0.f, 0.f, 0.f, 0.f}};
+#pragma unroll
+    for (int ks = 0; ks < TM / 4; ++ks) {
+        const int r = 4 * ks + lq;
+        const float a = Xs[r * XS + 16 * it + li];
+#pragma unroll
+        for (int u = 0; u < 2; ++u)
+            p[u] = __builtin_amdgcn_mfma_f32_16x16x4f32(a, Gs[r * GS + ub + 16 * u + li], p[u], 0, 0, 0);
+    }
+    // lane (li, lq) holds P[input 16 it + 4 lq + v][unit ub + 16 u + li]
+    float *dst = g.dw1 + (int64_t)bx * g.dw1_split + (int64_t)by * TN;
+#pragma unroll
+    for (int u = 0; u < 2; ++u)
+#pragma unroll
+        for (int v = 0; v < 4; ++v)
+            dst[(int64_t)(16 * it + 4 * lq + v) * g.N + ub + 16 * u + li] = p[u][v];
 }
 
 // One output tile (bx, by) of split bz; lds holds gemm_lds_floats(TM, TN, BF3).
@@ -326,8 +389,9 @@ __device__ __forceinline__ void gemm_block(const GemmArgs &g, int bx, int by, in
         gemm_fetch<OP, TM, TN, BF3>(st[q], A, lda, B, ldb, M, N, m0, n0, kb + q * GK, ke, t);
     // the mask of the epilogue, loaded now (clamped addresses, no lane condition)
     // so that its loads overlap the K loop instead of each waiting at the end
-    float gm[EP == EP_MASK ? MI : 1][EP == EP_MASK ? NJ : 1][4];
-    if constexpr (EP == EP_MASK) {
+    constexpr bool MASKED = EP == EP_MASK || EP == EP_MASK_DW1;
+    float gm[MASKED ? MI : 1][MASKED ? NJ : 1][4];
+    if constexpr (MASKED) {
 #pragma unroll
         for (int i = 0; i < MI; ++i)
 #pragma unroll
@@ -431,15 +495,20 @@ __device__ __forceinline__ void gemm_block(const GemmArgs &g, int bx, int by, in
 #pragma unroll
             for (int v = 0; v < 4; ++v) {
                 const int64_t m = m0 + wm * (TM / 2) + i * 16 + 4 * lq + v;
-                if (m >= M || n >= N) continue;
+                if (m >= M || n >= N) {
+                    if constexpr (EP == EP_MASK_DW1) acc[i][j][v] = 0.0f;   // no row: no term
+                    continue;
+                }
                 float r = BF3 ? acc[i][j][v] + lo[i][j][v] : acc[i][j][v];
                 // eq. 12; a NaN passes (a diverged step must reach the loss: an
                 // infinite operand leaves NaN in its split parts)
                 if constexpr (EP == EP_RELU) r = r <= 0.0f ? 0.0f : r;
-                if constexpr (EP == EP_MASK) r = gm[i][j][v] > 0.0f ? r : 0.0f;    // eq. 17
+                if constexpr (MASKED) r = gm[i][j][v] > 0.0f ? r : 0.0f;    // eq. 17
+                if constexpr (EP == EP_MASK_DW1) acc[i][j][v] = r;
                 Cz[m * ldc + n] = r;
             }
         }
+    if constexpr (EP == EP_MASK_DW1) dw1_partial<TM, TN, MI, NJ>(g, bx, by, acc, lds);
 }
 
 template <int OP, int EP, int TM, int TN, bool BF3>
@@ -715,7 +784,11 @@ static bool deep_shape_ok(int32_t d_in, int32_t hidden, int32_t layers) {
 // the count at max_batch sizes the partial buffer for every batch.
 static int64_t seg_chunks(int h, int L, int64_t nb, int s) {
     int64_t splits;
-    if (s < L) {
+    if (s == 0 && L > 1) {
+        // dW_1 comes from the epilogue of the back-propagation into layer 1,
+        // one partial per row tile of that product (32 or 64 rows)
+        splits = (nb + 31) / 32;
+    } else if (s < L) {
         const int64_t K = s == 0 ? D_IN : h;
         const int64_t tiles = ((K + GT - 1) / GT) * (h / GT);
         splits = (512 + tiles - 1) / tiles;
@@ -744,13 +817,16 @@ static int64_t part_layout(int h, int L, int64_t mb, int64_t *off) {
 // The plan of a batch of nb rows: chunk length rounded up to the GEMM's K chunk
 // (to the output kernel's pass for w_o), and the chunk count that length gives
 // (never more than seg_chunks).
-static void split_plan(int h, int L, int64_t nb, const int64_t *part_off, SplitPlan *sp) {
+// dw1_rows: with more than one layer, the rows of one back-propagation tile
+// into layer 1, whose epilogue writes one dW_1 partial per row tile.
+static void split_plan(int h, int L, int64_t nb, const int64_t *part_off, int dw1_rows, SplitPlan *sp) {
     sp->nseg = L + 1;
     for (int s = 0; s <= L; ++s) {
         const int64_t splits = seg_chunks(h, L, nb, s);
         int64_t c = (nb + splits - 1) / splits;
         const int64_t q = s < L ? GK : OUT_ROWS;
         c = (c + q - 1) / q * q;
+        if (s == 0 && L > 1) c = dw1_rows;
         sp->kc[s] = c;
         sp->splits[s] = (int)((nb + c - 1) / c);
         sp->seg_end[s] = s < L ? layer_offset(h, s + 2) : deep_np(h, L);
@@ -795,6 +871,9 @@ static GemmArgs gemm_args(const float *A, int lda, const float *B, int ldb, floa
     g.kc = kc;
     g.G = G;
     g.ldg = ldg;
+    g.X = nullptr;
+    g.dw1 = nullptr;
+    g.dw1_split = 0;
     g.gx = (int)((M + tm - 1) / tm);
     g.gy = (N + GT - 1) / GT;
     g.gz = splits;
@@ -913,8 +992,16 @@ static hipError_t deep_step(DeepCtx &c, const float *X, int64_t n_rows, const fl
     const float *HL = c.H + (int64_t)(L - 1) * mbh;
     const float *wo = c.params + layer_offset(h, L + 1);
     int cur = 0;
+    // with more than one layer, dW_1 comes from the epilogue of the
+    // back-propagation into layer 1 (one partial per row tile of that product)
+    int dw1_rows = 0;
+    if (L > 1) {
+        bool small;
+        (void)gemm_args(c.G[0], h, c.params, h, c.G[1], h, 0, nb, h, h, 1, h, c.Xb, h, &small);
+        dw1_rows = small ? 32 : GT;
+    }
     SplitPlan sp;
-    split_plan(h, L, nb, c.part_off, &sp);
+    split_plan(h, L, nb, c.part_off, dw1_rows, &sp);
     // output layer: r^2, G_L and the dw_o partials of each row chunk
     DEEP_TRY(launch_out(c, HL, wo, nb, sp.kc[L], sp.splits[L], c.part + sp.part_off[L]));
     for (int l = L; l >= 1; --l) {
@@ -928,12 +1015,20 @@ static hipError_t deep_step(DeepCtx &c, const float *X, int64_t n_rows, const fl
         if (l > 1) {
             // G_{l-1} = (G_l W_l^T) (.) [H_{l-1} > 0], eq. 17 one layer down; it
             // reads G_l as the weight gradient does and writes the other buffer,
-            // so the two products share one launch
-            const GemmArgs gg = gemm_args(c.G[cur], h, c.params + layer_offset(h, l), h, c.G[cur ^ 1], h,
-                                          0, nb, h, h, 1, h, Hin, h, &s2);
-            DEEP_TRY((gemm_pair<OP_TN, EP_NONE, OP_NT, EP_MASK>(c.stream, gw, s1, gg, s2)));
+            // so the two products share one launch. Into layer 1 (l = 2) its
+            // epilogue also forms the row tile's partial of dW_1 = X^T G_1.
+            GemmArgs gg = gemm_args(c.G[cur], h, c.params + layer_offset(h, l), h, c.G[cur ^ 1], h,
+                                    0, nb, h, h, 1, h, Hin, h, &s2);
+            if (l == 2) {
+                gg.X = c.Xb;
+                gg.dw1 = c.part + sp.part_off[0];
+                gg.dw1_split = (int64_t)D_IN * h;
+                DEEP_TRY((gemm_pair<OP_TN, EP_NONE, OP_NT, EP_MASK_DW1>(c.stream, gw, s1, gg, s2)));
+            } else {
+                DEEP_TRY((gemm_pair<OP_TN, EP_NONE, OP_NT, EP_MASK>(c.stream, gw, s1, gg, s2)));
+            }
             cur ^= 1;
-        } else {
+        } else if (L == 1) {
             DEEP_TRY((gemm<OP_TN, EP_NONE>(c.stream, Hin, K, c.G[cur], h, c.part + sp.part_off[l - 1], h,
                                            (int64_t)K * h, K, h, nb, sp.splits[l - 1], sp.kc[l - 1])));
         }
