@@ -669,7 +669,7 @@ __global__ __launch_bounds__(256) void k_deep_apply(const float *__restrict__ pa
                                                     float *__restrict__ dparams, float lr, int sgd,
                                                     const float *__restrict__ sq, int64_t nb,
                                                     ReduceArgs ra, const GatherArgs next) {
-    constexpr int U = 32;     // loads in flight per lane; the adds stay in index order
+    constexpr int U = 32;     // loads of one batch per lane; the adds stay in index order
     if ((int)blockIdx.x > napply) {
         gather_one(next, (int64_t)(blockIdx.x - napply - 1) * 256 + threadIdx.x);
         return;
@@ -724,6 +724,17 @@ __global__ __launch_bounds__(256) void k_deep_apply(const float *__restrict__ pa
     const float w = sgd ? params[p] : 0.0f;
     float v = 0.0f;
     int z0 = 0;
+    for (; z0 + 2 * U <= n; z0 += 2 * U) {   // two batches of loads in flight, added in order
+        float x[U], y[U];
+#pragma unroll
+        for (int j = 0; j < U; ++j) x[j] = q[(int64_t)(z0 + j) * size];
+#pragma unroll
+        for (int j = 0; j < U; ++j) y[j] = q[(int64_t)(z0 + U + j) * size];
+#pragma unroll
+        for (int j = 0; j < U; ++j) v += x[j];
+#pragma unroll
+        for (int j = 0; j < U; ++j) v += y[j];
+    }
     for (; z0 + U <= n; z0 += U) {
         float x[U];
 #pragma unroll
