@@ -142,8 +142,12 @@ __global__ __launch_bounds__(64 * FwdShape<H>::WAVES, FwdShape<H>::WAVES_PER_SIM
         for (int u = 0; u < NUT; ++u)
 #pragma unroll
             for (int v = 0; v < 4; ++v) {
-                const float z = acc[u][v];
-                yp[v] = fmaf(z > 0.0f ? z : 0.0f, w2v[u], yp[v]);
+                // ReLU as an integer max on the bits: every negative float
+                // (-0 included) has a negative pattern and becomes +0, every
+                // positive one stays; one instruction, where the float form
+                // costs two (a canonicalizing max first)
+                const float z = __int_as_float(max(__float_as_int(acc[u][v]), 0));
+                yp[v] = fmaf(z, w2v[u], yp[v]);
             }
         // lane li ends with row 4 lq + (li >> 2) summed over the 16 unit lanes
         const float rowv = rsum16x4(yp, li);
