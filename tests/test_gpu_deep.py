@@ -113,7 +113,7 @@ def _ctx(mlp, P, h, L, max_batch):
 
 # --- forward -------------------------------------------------------------------
 
-@pytest.mark.parametrize("h,L", [(64, 1), (64, 2), (64, 3), (128, 2)])
+@pytest.mark.parametrize("h,L", [(64, 1), (64, 2), (64, 3), (128, 2), (192, 2)])
 def test_forward_dyadic_is_exact(mlp, h, L):
     rng = np.random.default_rng(10 * h + L)
     X, Y, P = _dyadic(rng, 1000, h, L)
@@ -213,6 +213,39 @@ def test_gradients_gaussian_wide_tiles(mlp):
     e = rel(dP.cpu().numpy(), ref)
     print("kink-free batch of %d rows at h = 1024: gradient rel %.3e" % (B, e))
     assert e <= 1e-5
+    mlp.mlp_deep_check_errors(ctx)
+
+
+@pytest.mark.parametrize("h", [192, 320, 960])
+def test_widths_off_the_power_of_two_grid(mlp, h):
+    """Hidden widths with an odd number of 64-unit tiles (3, 5, 15): the GEMM
+    grids' unit-tile counts, the output kernel's units per lane and the
+    update kernel's segment ends all differ from the power-of-two nets. At a
+    batch of 500 kink-free rows (ragged against every row tile): the forward at
+    1e-5, gradients and loss at 1e-5, and two SGD steps against the oracle's."""
+    L, B, lr = 2, 500, 0.002
+    rng = np.random.default_rng(h)
+    d = datagen.make_data(5000, 32, seed=6, with_perm=False)
+    P = _gauss_net(rng, h, L)
+    ctx, p = _ctx(mlp, P, h, L, B)
+    cand = rng.integers(0, 5000, size=8 * B).astype(np.int32)
+    rows = _kink_free(d.X, P, h, L, cand)[:B]
+    assert len(rows) == B, (len(rows), B)
+    got = mlp.mlp_deep_forward(ctx, _to(d.X), _to(rows)).cpu().numpy()
+    assert rel(got, oracle.deep_forward(d.X, P, D, h, L, idx=rows)) < 1e-5
+    dP, loss = mlp.mlp_deep_backward(ctx, _to(d.X), _to(d.Y), _to(rows))
+    ref, rL, _ = oracle.deep_grad(d.X, d.Y, P, D, h, L, idx=rows)
+    assert abs(float(loss.cpu()[0]) - rL) <= 1e-5 * rL
+    e = rel(dP.cpu().numpy(), ref)
+    print("h = %d, kink-free batch of %d rows: gradient rel %.3e" % (h, B, e))
+    assert e <= 1e-5
+    # two steps over a 1000-row set in identity order (batches of 500)
+    X2, Y2 = d.X[:1000], d.Y[:1000]
+    gP, gsl, _ = _train(mlp, X2, Y2, P, h, L, B, lr, 1, max_steps=2)
+    tr = oracle.deep_train(X2, Y2, P, D, h, L, B, lr, 1, max_steps=2)
+    P0 = P.astype(np.float64)
+    assert rel(gP - P0, tr["P"] - P0) <= 1e-3
+    assert np.all(np.abs(gsl - tr["step_loss"]) <= 1e-4 * tr["step_loss"])
     mlp.mlp_deep_check_errors(ctx)
 
 
