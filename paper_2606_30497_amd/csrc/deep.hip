@@ -410,36 +410,36 @@ __device__ __forceinline__ void gemm_block(const GemmArgs &g, int bx, int by, in
     // operand tile, for every part. The leading part product a0 b0 accumulates
     // in acc, the five smaller ones (below 2^-7 |a b| together) in lo, smallest
     // first, so that their roundings are relative to their own sum, not to the
-    // whole dot product; all tiles' product of one part pair go out back to
-    // back (independent accumulators).
+    // whole dot product. The B parts are read once per chunk and the A parts
+    // one row tile at a time (the registers of three workgroups per CU); each
+    // part pair's products of a row tile go out back to back (independent
+    // accumulators).
     auto mfma_chunk = [&](int buf) __attribute__((always_inline)) {
         if constexpr (BF3) {
             const uint16_t *As = reinterpret_cast<const uint16_t *>(As2[buf]);
             const uint16_t *Bs = reinterpret_cast<const uint16_t *>(Bs2[buf]);
-            u4v a[MI][3], b[NJ][3];
+            u4v b[NJ][3];
 #pragma unroll
-            for (int p = 0; p < 3; ++p) {
-#pragma unroll
-                for (int i = 0; i < MI; ++i)
-                    a[i][p] = *reinterpret_cast<const u4v *>(
-                        As + (p * TM + wm * (TM / 2) + i * 16 + li) * GK + swz(li, 8 * lq));
+            for (int p = 0; p < 3; ++p)
 #pragma unroll
                 for (int j = 0; j < NJ; ++j)
                     b[j][p] = *reinterpret_cast<const u4v *>(
                         Bs + (p * TN + wn * (TN / 2) + j * 16 + li) * GK + swz(li, 8 * lq));
-            }
             constexpr int PA[5] = {2, 1, 0, 1, 0}, PB[5] = {0, 1, 2, 0, 1};
 #pragma unroll
-            for (int q = 0; q < 5; ++q)
+            for (int i = 0; i < MI; ++i) {
+                u4v a[3];
 #pragma unroll
-                for (int i = 0; i < MI; ++i)
+                for (int p = 0; p < 3; ++p)
+                    a[p] = *reinterpret_cast<const u4v *>(
+                        As + (p * TM + wm * (TM / 2) + i * 16 + li) * GK + swz(li, 8 * lq));
 #pragma unroll
-                    for (int j = 0; j < NJ; ++j)
-                        lo[i][j] = mfma_bf16(a[i][PA[q]], b[j][PB[q]], lo[i][j]);
+                for (int q = 0; q < 5; ++q)
 #pragma unroll
-            for (int i = 0; i < MI; ++i)
+                    for (int j = 0; j < NJ; ++j) lo[i][j] = mfma_bf16(a[PA[q]], b[j][PB[q]], lo[i][j]);
 #pragma unroll
-                for (int j = 0; j < NJ; ++j) acc[i][j] = mfma_bf16(a[i][0], b[j][0], acc[i][j]);
+                for (int j = 0; j < NJ; ++j) acc[i][j] = mfma_bf16(a[0], b[j][0], acc[i][j]);
+            }
         } else {
             const float *As = As2[buf], *Bs = Bs2[buf];
 #pragma unroll
@@ -511,8 +511,10 @@ __device__ __forceinline__ void gemm_block(const GemmArgs &g, int bx, int by, in
     if constexpr (EP == EP_MASK_DW1) dw1_partial<TM, TN, MI, NJ>(g, bx, by, acc, lds);
 }
 
+// The bf16x3 tiles are compiled for three workgroups per CU (the most their LDS
+// allows; about 168 registers a lane), the fp32 ones without a bound.
 template <int OP, int EP, int TM, int TN, bool BF3>
-__global__ __launch_bounds__(256) void k_gemm(const GemmArgs g) {
+__global__ __launch_bounds__(256, BF3 ? 3 : 1) void k_gemm(const GemmArgs g) {
     __shared__ __attribute__((aligned(16))) float lds[gemm_lds_floats(TM, TN, BF3)];
     gemm_block<OP, EP, TM, TN, BF3>(g, blockIdx.x, blockIdx.y, blockIdx.z, lds);
 }
@@ -521,7 +523,7 @@ __global__ __launch_bounds__(256) void k_gemm(const GemmArgs g) {
 // [0, g1.gx g1.gy g1.gz) compute the first, the rest the second. With both
 // resident together the CUs hold twice the workgroups of either alone.
 template <int OP1, int EP1, int TM1, int TN1, int OP2, int EP2, int TM2, int TN2, bool BF3>
-__global__ __launch_bounds__(256) void k_gemm_pair(const GemmArgs g1, const GemmArgs g2) {
+__global__ __launch_bounds__(256, BF3 ? 3 : 1) void k_gemm_pair(const GemmArgs g1, const GemmArgs g2) {
     constexpr int L1 = gemm_lds_floats(TM1, TN1, BF3), L2 = gemm_lds_floats(TM2, TN2, BF3);
     __shared__ __attribute__((aligned(16))) float lds[L1 > L2 ? L1 : L2];
     const int n1 = g1.gx * g1.gy * g1.gz;
