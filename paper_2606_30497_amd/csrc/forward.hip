@@ -47,8 +47,11 @@ struct FwdShape {
     static constexpr int RT = H == 32 ? 2 : 1;
     // waves per SIMD the register budget allows (a wave holds 13 registers per
     // unit tile of weights and 4 of accumulators, and about 40 more): small
-    // nets need more waves in flight to keep enough row loads outstanding
-    static constexpr int WAVES_PER_SIMD = NUT <= 2 ? 6 : NUT <= 4 ? 4 : WPT == 1 ? 3 : 2;
+    // nets need more waves in flight to keep enough row loads outstanding; at
+    // 128 units a wave, three (168 registers, a few of them spilled) beat two
+    // (172) where a workgroup's waves fit three times, i.e. except at h = 1024
+    // (eight waves a workgroup)
+    static constexpr int WAVES_PER_SIMD = NUT <= 2 ? 6 : NUT <= 4 ? 4 : WPT == 8 ? 2 : 3;
     static_assert(H % 16 == 0 && WPT * UW == H && WPT <= 8, "shape");
 };
 
