@@ -790,8 +790,10 @@ static bool deep_shape_ok(int32_t d_in, int32_t hidden, int32_t layers) {
 }
 
 // Row chunks of segment s's gradient before rounding the chunk length: a weight
-// segment W_l gets enough chunks for its GEMM to reach about 512 workgroups
-// (output tiles x chunks), at most SPLIT_MAX, with at least 64 rows a chunk; w_o
+// segment W_l gets enough chunks for its GEMM to reach about 256 workgroups
+// (output tiles x chunks) at h <= 256 and 512 above, at most SPLIT_MAX, with at
+// least 64 rows a chunk (at h = 256 and batch 4096: 16 chunks of 256 rows, the
+// back-propagation's K, so both products of a pair run eight K chunks); w_o
 // gets one chunk per OUT_ROWS rows of the output kernel, at most OUT_CHUNKS_MAX. This
 // count never falls as nb grows, and the chunks a plan uses never exceed it, so
 // the count at max_batch sizes the partial buffer for every batch.
@@ -804,7 +806,8 @@ static int64_t seg_chunks(int h, int L, int64_t nb, int s) {
     } else if (s < L) {
         const int64_t K = s == 0 ? D_IN : h;
         const int64_t tiles = ((K + GT - 1) / GT) * (h / GT);
-        splits = (512 + tiles - 1) / tiles;
+        const int64_t target = h <= 256 ? 256 : 512;
+        splits = (target + tiles - 1) / tiles;
         const int64_t by_rows = (nb + 63) / 64;
         if (splits > by_rows) splits = by_rows;
         splits = splits > SPLIT_MAX ? SPLIT_MAX : splits;
