@@ -42,16 +42,16 @@ struct FwdShape {
     static constexpr int WPT = H / UW;             // waves per row tile: 1, 2, 4 or 8
     static constexpr int WAVES = WPT > 4 ? WPT : 4;   // waves per workgroup
     static constexpr int TPI = WAVES / WPT;        // row-tile slots per workgroup iteration
-    // row tiles per slot and iteration: the HBM-bound h = 32 keeps two tiles of
-    // loads in flight per wave
-    static constexpr int RT = H == 32 ? 2 : 1;
+    // row tiles per slot and iteration: the HBM-bound h = 32 keeps four tiles
+    // of loads in flight per wave (at four waves a SIMD)
+    static constexpr int RT = H == 32 ? 4 : 1;
     // waves per SIMD the register budget allows (a wave holds 13 registers per
-    // unit tile of weights and 4 of accumulators, and about 40 more): small
-    // nets need more waves in flight to keep enough row loads outstanding; at
+    // unit tile of weights and 4 of accumulators, about 40 more, and 8 per row
+    // tile in flight): small nets need enough row loads outstanding; at
     // 128 units a wave, three (168 registers, a few of them spilled) beat two
     // (172) where a workgroup's waves fit three times, i.e. except at h = 1024
     // (eight waves a workgroup)
-    static constexpr int WAVES_PER_SIMD = NUT <= 2 ? 6 : NUT <= 4 ? 4 : WPT == 8 ? 2 : 3;
+    static constexpr int WAVES_PER_SIMD = NUT <= 4 ? 4 : WPT == 8 ? 2 : 3;
     static_assert(H % 16 == 0 && WPT * UW == H && WPT <= 8, "shape");
 };
 
