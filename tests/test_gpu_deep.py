@@ -249,6 +249,30 @@ def test_widths_off_the_power_of_two_grid(mlp, h):
     mlp.mlp_deep_check_errors(ctx)
 
 
+def test_large_batch_split_plans(mlp):
+    """A batch of 20,000 kink-free rows at 32-256x2-1: the back-propagation runs
+    64 x 64 tiles beside a weight gradient on 32 x 64 tiles (16 row chunks of
+    1280 rows, the last one ragged) in one launch, dW_1 comes in 313 partials
+    (one per 64-row tile), and the output layer in 209 chunks of 96 rows (its
+    cap of 256 chunks reached), so the update kernel's loops run many batches
+    and a tail. Gradient and loss at 1e-5."""
+    h, L, B = 256, 2, 20000
+    rng = np.random.default_rng(20000)
+    d = datagen.make_data(60000, 32, seed=8, with_perm=False)
+    P = _gauss_net(rng, h, L)
+    ctx, _ = _ctx(mlp, P, h, L, B)
+    cand = rng.integers(0, 60000, size=2 * B).astype(np.int32)
+    rows = _kink_free(d.X, P, h, L, cand)[:B]
+    assert len(rows) == B, (len(rows), B)
+    dP, loss = mlp.mlp_deep_backward(ctx, _to(d.X), _to(d.Y), _to(rows))
+    ref, rL, _ = oracle.deep_grad(d.X, d.Y, P, D, h, L, idx=rows)
+    assert abs(float(loss.cpu()[0]) - rL) <= 1e-5 * rL
+    e = rel(dP.cpu().numpy(), ref)
+    print("kink-free batch of %d rows: gradient rel %.3e" % (B, e))
+    assert e <= 1e-5
+    mlp.mlp_deep_check_errors(ctx)
+
+
 @pytest.mark.parametrize("h,L", [(64, 8), (128, 8)])
 @pytest.mark.parametrize("B", [7, 160, 1000])
 def test_gradients_gaussian_eight_layers(mlp, h, L, B):
