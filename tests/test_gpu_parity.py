@@ -558,6 +558,26 @@ def test_launch_info_single_launch(mlp):
     assert launches == 2 * 3 * 3 + 1
 
 
+def test_batch_beyond_the_fused_shapes_runs_the_tile_path(mlp):
+    """A batch of 6,000 rows at h = 256 is more than any fused trainer shape
+    holds (4,096 rows), so mlp_train_epochs under the default strategy runs the
+    tile path (two launches a step): one shuffled epoch of 20,000 rows (four
+    steps, the last batch 2,000 rows) against the oracle at the main bars."""
+    n, h, B, lr = 20000, 256, 6000, 0.002
+    d = datagen.make_data(n, h, epochs=1, shuffle=True, seed=66)
+    ctx, w1, w2 = _ctx(mlp, d.W1, d.W2, B)
+    wg, launches = mlp.mlp_launch_info(ctx, n, B, 1)
+    assert launches == 2 * 4 + 1, launches
+    g1, g2, gsl, gel = _train_gpu(mlp, d, B, lr, 1, perm=d.perm)
+    ref = oracle.train(d.X, d.Y, d.W1, d.W2, B, lr, 1, perm=d.perm)
+    assert ref["steps"] == 4 and len(gsl) == 4
+    W10, W20 = d.W1.astype(np.float64), d.W2.astype(np.float64)
+    check("W1 - W1_0", g1 - W10, ref["W1"] - W10, 1e-3)
+    check("W2 - W2_0", g2 - W20, ref["W2"] - W20, 1e-3)
+    assert np.all(np.abs(gsl - ref["step_loss"]) <= 1e-3 * np.abs(ref["step_loss"]))
+    assert abs(gel[0] - ref["epoch_loss"][0]) <= 1e-3 * ref["epoch_loss"][0]
+
+
 def test_workspace_reused_by_a_new_context(mlp):
     """A workspace that held another context's exchange words must not leak them
     into a new context (regression: stale step tags matched the new call's tags)."""
