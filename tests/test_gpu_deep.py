@@ -394,6 +394,21 @@ def test_train_gaussian_workload_batch(mlp):
     assert np.all(np.abs(gsl - ref["step_loss"]) <= 1e-4 * ref["step_loss"])
 
 
+def test_zero_learning_rate(mlp):
+    """lr = 0: the parameters stay bitwise as they were through a shuffled epoch
+    (four steps, the last one a tail) and every step's loss is the batch MSE at
+    the initial parameters, as the oracle's run with lr = 0 gives it."""
+    h, L, B = 256, 2, 1000
+    d = datagen.make_data(3400, 32, epochs=1, seed=77)
+    P = _gauss_net(np.random.default_rng(77), h, L)
+    gP, gsl, gel = _train(mlp, d.X, d.Y, P, h, L, B, 0.0, 1, perm=d.perm)
+    assert np.array_equal(gP, P)
+    ref = oracle.deep_train(d.X, d.Y, P, D, h, L, B, 0.0, 1, perm=d.perm)
+    assert ref["steps"] == 4 and len(gsl) == 4
+    assert np.all(np.abs(gsl - ref["step_loss"]) <= 1e-5 * ref["step_loss"])
+    assert abs(gel[0] - ref["epoch_loss"][0]) <= 1e-5 * ref["epoch_loss"][0]
+
+
 def test_deterministic(mlp):
     rng = np.random.default_rng(3)
     d = datagen.make_data(3000, 32, epochs=2, seed=8)

@@ -578,6 +578,21 @@ def test_batch_beyond_the_fused_shapes_runs_the_tile_path(mlp):
     assert abs(gel[0] - ref["epoch_loss"][0]) <= 1e-3 * ref["epoch_loss"][0]
 
 
+@pytest.mark.parametrize("h,B", [(256, 4096), (1024, 1024), (32, 256)])
+def test_zero_learning_rate(mlp, h, B):
+    """lr = 0 (eq. 19 with a zero step): every step leaves W1 and W2 bitwise as
+    they were, and each step's reported loss is the batch MSE at the initial
+    weights (eq. 14), which the oracle's run with lr = 0 gives step by step."""
+    n = 3 * B + B // 3
+    d = datagen.make_data(n, h, epochs=1, shuffle=True, seed=h + B)
+    g1, g2, gsl, gel = _train_gpu(mlp, d, B, 0.0, 1, perm=d.perm)
+    assert np.array_equal(g1, d.W1) and np.array_equal(g2, d.W2)
+    ref = oracle.train(d.X, d.Y, d.W1, d.W2, B, 0.0, 1, perm=d.perm)
+    assert ref["steps"] == 4 and len(gsl) == 4
+    assert np.all(np.abs(gsl - ref["step_loss"]) <= 1e-5 * ref["step_loss"])
+    assert abs(gel[0] - ref["epoch_loss"][0]) <= 1e-5 * ref["epoch_loss"][0]
+
+
 def test_workspace_reused_by_a_new_context(mlp):
     """A workspace that held another context's exchange words must not leak them
     into a new context (regression: stale step tags matched the new call's tags)."""
